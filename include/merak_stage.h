@@ -1,0 +1,251 @@
+/*
+ * merak_stage.h: C ABI of the MI355X (gfx950) stage-shard library.
+ *
+ * One GPU's share of a GPT pipeline stage: L consecutive transformer blocks
+ * (a pipeline stage is a contiguous run of blocks, paper Sec. 2 "Pipeline
+ * model parallelism" and Sec. 4.2), each cut Megatron-style into a
+ * tensor-model-parallel shard (Sec. 2 "Tensor model parallelism"; Sec. 4.1):
+ * column-parallel QKV and FC1, causal attention on the shard's heads,
+ * row-parallel projection and FC2.  A block has two AllReduces in the forward
+ * pass and two in the backward pass (Sec. 5.3).  On one GPU each AllReduce is
+ * the identity; the value this shard would contribute to it (its partial sum)
+ * is written to a caller-supplied hand-off buffer.
+ *
+ * The method's two schedule features are carried by the kernels' schedule:
+ *   - sub-pipelined TMP (Sec. 5.3): each micro-batch is split evenly along the
+ *     batch axis into n independent sub-micro-batches that run on two HIP
+ *     streams, so one slice's GEMMs overlap another slice's other work;
+ *   - stage-aware recomputation (Sec. 5.2): a per-block mask selects blocks
+ *     that keep only their input; their activations are rebuilt by
+ *     merak_stage_recompute, which needs no upstream gradient and may run
+ *     early, before the gradient arrives (Sec. 5.1, early recomputation).
+ *
+ * Block math (pre-LN GPT block; internals are not fixed by the paper):
+ *   ln1 = LN1(x);  qkv = ln1 W_qkv^T + b_qkv  ([q|k|v] x local heads x d)
+ *   O   = softmax(q k^T / sqrt(d), causal) v;  p_o = O W_o^T   (partial)
+ *   x1  = x + R(p_o) + b_o;  ln2 = LN2(x1);  u = ln2 W1^T + b1;  g = GeLU_tanh(u)
+ *   p_f = g W2^T (partial);  y = x1 + R(p_f) + b2;  R = identity on one GPU.
+ * LayerNorm: biased variance, eps inside the square root, fp32 statistics.
+ *
+ * Conventions for every entry point
+ *   - Return value: MERAK_OK (0) or a negative merak_status.  Argument, shape,
+ *     alignment, workspace and call-order errors are detected on the host
+ *     before anything is enqueued; such a call has no side effects.
+ *   - Device pointers are caller-owned (allocated by the caller, for example
+ *     as torch tensors); the library never allocates device memory.  Every
+ *     device pointer must be 16-byte aligned; workspaces 256-byte aligned.
+ *   - Streams are hipStream_t values passed as void* (NULL = the null
+ *     stream); stream0 and stream1 may be equal.  Calls enqueue work and
+ *     return; all work of a call is ordered after prior work on stream0 and
+ *     stream1, and its completion is recorded on stream0 (stream0 waits for
+ *     stream1 before the call returns).  Kernel faults surface at the
+ *     caller's next synchronisation, as usual in HIP.
+ *   - Element types: MERAK_BF16 = bf16 activations/weights with fp32
+ *     accumulation; MERAK_FP32 = the fp32 check mode (every tensor fp32).
+ *     Weight gradients are always fp32.
+ *   - Layouts are row-major.  Activations are [micro_batch, seq_len, features].
+ *     Weights are stored [out, in]: a linear layer computes X W^T + b.
+ */
+#ifndef MERAK_STAGE_H
+#define MERAK_STAGE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MERAK_OK = 0,
+  MERAK_ERR_INVALID_ARG = -1, /* NULL handle/pointer, bad enum, bad flag        */
+  MERAK_ERR_SHAPE = -2,       /* dimensions violate the constraints below       */
+  MERAK_ERR_ORDER = -3,       /* call-order violation (see merak_stage_bwd)     */
+  MERAK_ERR_ALIGN = -4,       /* device pointer not 16-byte (256 for workspaces)*/
+  MERAK_ERR_WORKSPACE = -5,   /* workspace smaller than the size query returned */
+  MERAK_ERR_HIP = -6,         /* a HIP runtime call failed                      */
+  MERAK_ERR_UNSUPPORTED = -7  /* valid but not implemented (e.g. head_dim)     */
+} merak_status;
+
+typedef enum { MERAK_BF16 = 0, MERAK_FP32 = 1 } merak_dtype;
+
+/* Number of parameter tensors per block, in flat-buffer order:
+ *   0 ln1_g[h]   1 ln1_b[h]   2 w_qkv[3h/t, h]   3 b_qkv[3h/t]
+ *   4 w_o[h, h/t]             5 b_o[h]
+ *   6 ln2_g[h]   7 ln2_b[h]   8 w1[f/t, h]       9 b1[f/t]
+ *  10 w2[h, f/t]             11 b2[h]
+ * The shard map (which rows/columns of the full model a rank owns) is
+ * Megatron's: rank r owns heads [r a/t, (r+1) a/t) -- its w_qkv rows are its
+ * q rows, then its k rows, then its v rows -- and FFN units [r f/t, (r+1) f/t).
+ * LayerNorm parameters, b_o and b2 are replicated; a row-parallel bias is
+ * added once, after the reduction. */
+#define MERAK_PARAMS_PER_BLOCK 12
+
+/* Stage configuration.  Dimensions are those of the full (t = 1) model.
+ * Constraints (else MERAK_ERR_SHAPE): 1 <= n_blocks <= 64; n_heads % tp_degree
+ * == 0; hidden % n_heads == 0; ffn % tp_degree == 0; micro_batch %
+ * n_sub_microbatches == 0; hidden, hidden/tp_degree, ffn/tp_degree and
+ * seq_len multiples of 64; recompute_mask has no bit >= n_blocks; ln_eps > 0.
+ * head_dim = hidden/n_heads must be 64, 96 or 128 (else MERAK_ERR_UNSUPPORTED). */
+typedef struct {
+  int32_t n_blocks;           /* L: blocks in the stage                               */
+  int32_t hidden;             /* h                                                    */
+  int32_t n_heads;            /* a (global)                                           */
+  int32_t ffn;                /* f (global)                                           */
+  int32_t seq_len;            /* s                                                    */
+  int32_t micro_batch;        /* b                                                    */
+  int32_t tp_degree;          /* t: local heads a/t, local FFN width f/t              */
+  int32_t n_sub_microbatches; /* n: even split of the micro-batch (Sec. 5.3)          */
+  uint64_t recompute_mask;    /* bit l: block l keeps only its input (Sec. 5.2)       */
+  int32_t dtype;              /* merak_dtype                                          */
+  float ln_eps;               /* LayerNorm epsilon (1e-5)                             */
+} merak_stage_config;
+
+typedef struct merak_stage* merak_stage_t;
+
+/* Human-readable name of a status code (static string). */
+const char* merak_status_str(int status);
+
+/* Host-only check of a configuration; no GPU needed. */
+int merak_stage_validate(const merak_stage_config* cfg);
+
+/* Parameter layout of one rank's stage shard.  *total_elems receives the element
+ * count of the flat parameter buffer (elements of the config's dtype) and of the
+ * fp32 gradient buffer (same layout).  If offsets is not NULL it receives
+ * n_blocks * MERAK_PARAMS_PER_BLOCK element offsets, block-major, in the order
+ * listed above.  Every offset is a multiple of 64 elements.  Host-only. */
+int merak_stage_param_layout(const merak_stage_config* cfg, size_t* total_elems, size_t* offsets);
+
+/* Device memory a handle needs (host-only query).
+ *   *workspace_bytes: per-handle memory (activations kept for the backward pass
+ *      of the blocks that are not recomputed, inputs of recomputed blocks, and
+ *      backward scratch);
+ *   *recompute_bytes: activations of the recomputed blocks (0 when the mask is
+ *      0).  Handles that never have a recompute->bwd window open at the same
+ *      time may share one recompute area.
+ * Either output pointer may be NULL. */
+int merak_stage_workspace_bytes(const merak_stage_config* cfg, size_t* workspace_bytes,
+                                size_t* recompute_bytes);
+
+/* Create a handle bound to a configuration and caller-owned device memory.
+ * The workspace must hold at least *workspace_bytes and stays owned by the
+ * caller; it must not be freed before merak_stage_destroy.  recompute_area may
+ * be NULL when recompute_bytes is 0.  Needs the GPU (creates HIP events on the
+ * current device).  On success *out receives the handle. */
+int merak_stage_create(const merak_stage_config* cfg, void* workspace, size_t workspace_bytes,
+                       void* recompute_area, size_t recompute_bytes, merak_stage_t* out);
+
+/* Destroy a handle (waits for nothing; the caller synchronises first). */
+int merak_stage_destroy(merak_stage_t stage);
+
+/* Forward pass of the stage for one micro-batch.
+ *   params        [total_elems] (dtype): the shard's parameters, layout above.
+ *   x             [b, s, h] (dtype): stage input.  It is read again by
+ *                 merak_stage_recompute and merak_stage_bwd, so it must stay
+ *                 unchanged until that backward work has completed.
+ *   y             [b, s, h] (dtype): stage output.
+ *   fwd_partials  NULL or [L][2][b, s, h] (dtype): hand-off buffers; [l][0] is
+ *                 block l's projection partial p_o, [l][1] its FC2 partial p_f
+ *                 (the inputs the two forward AllReduces would reduce).
+ * Sub-micro-batch j (samples [j b/n, (j+1) b/n)) runs on stream (j mod 2).
+ * Starts a new micro-batch: earlier activations of this handle are dropped. */
+int merak_stage_fwd(merak_stage_t stage, const void* params, const void* x, void* y,
+                    void* fwd_partials, void* stream0, void* stream1);
+
+/* Rebuild the activations of every block whose recompute bit is set, from the
+ * block inputs kept by merak_stage_fwd, into the recompute area.  Results are
+ * bit-identical to what the forward pass computed.  Needs no upstream gradient
+ * (early recomputation).  MERAK_ERR_ORDER if no forward pass is pending.  A
+ * no-op (MERAK_OK) when the mask is 0.  params must hold the same values as in
+ * the forward call. */
+int merak_stage_recompute(merak_stage_t stage, const void* params, void* stream0, void* stream1);
+
+/* Backward pass of the stage for the pending micro-batch.
+ *   dy            [b, s, h] (dtype): gradient of the stage output.
+ *   dx            [b, s, h] (dtype): gradient of the stage input.
+ *   grads         [total_elems] fp32: parameter gradients, same layout as params;
+ *                 overwritten when accumulate = 0, added to when accumulate = 1.
+ *   bwd_partials  NULL or [L][2][b, s, h] (dtype): [l][0] = block l's partial of
+ *                 the LN1-output gradient (dqkv W_qkv), [l][1] = the partial of
+ *                 the LN2-output gradient (du W1): the inputs of the two backward
+ *                 AllReduces.
+ * Weight gradients are computed per block over the whole micro-batch once all
+ * its sub-micro-batches are done (deterministic; no floating-point atomics).
+ * MERAK_ERR_ORDER if no forward pass is pending, if the mask is nonzero and
+ * merak_stage_recompute has not run since the forward pass, or if another
+ * handle has recomputed into a shared recompute area since.  Consumes the
+ * pending micro-batch. */
+int merak_stage_bwd(merak_stage_t stage, const void* params, const void* dy, void* dx,
+                    float* grads, int accumulate, void* bwd_partials, void* stream0,
+                    void* stream1);
+
+/* ------------------------------------------------------------------------
+ * Per-kernel entry points (each launches one hot-path kernel on `stream`).
+ * They exist so each kernel can be checked and timed on its own; the stage
+ * calls above use the same kernels.  dtype is merak_dtype; pointers follow the
+ * conventions above (16-byte aligned).  No entry point allocates memory.
+ * ---------------------------------------------------------------------- */
+
+/* GEMM epilogues. */
+typedef enum {
+  MERAK_EPI_STORE = 0,      /* C = acc                                               (dtype) */
+  MERAK_EPI_BIAS = 1,       /* C = acc + bias[n]                                     (dtype) */
+  MERAK_EPI_BIAS_GELU = 2,  /* aux = u = acc + bias[n];  C = GeLU_tanh(u)            (dtype) */
+  MERAK_EPI_BIAS_RESID = 3, /* aux = acc (skipped if aux is NULL); C = resid + acc + bias[n] */
+  MERAK_EPI_GELU_BWD = 4,   /* C = acc * GeLU_tanh'(aux), aux holding the stored u   (dtype) */
+  MERAK_EPI_F32 = 5         /* fp32 C = acc, or C += acc when accumulate = 1                 */
+} merak_epilogue;
+
+/* GEMM of the shard's linear layers: C[M,N] = op(A)[M,K] * op(B)[K,N], fp32
+ * accumulation (bf16 MFMA in MERAK_BF16 mode).
+ *   a_trans = 0: A[m,k] at a[m*lda + k];  1: A[m,k] at a[k*lda + m].
+ *   b_trans = 0: B[k,n] at b[n*ldb + k] (a weight [N,K]: "X W^T");
+ *             1: B[k,n] at b[k*ldb + n].
+ * M, N, K must be multiples of 64 and lda, ldb multiples of 8 (else
+ * MERAK_ERR_SHAPE).  C, resid and aux are [M, N] row-major (ld = N); bias is
+ * [N].  Elements are of `dtype` except C for MERAK_EPI_F32 (always fp32). */
+int merak_gemm(int dtype, int a_trans, int b_trans, int epilogue, int M, int N, int K,
+               const void* a, int lda, const void* b, int ldb, void* c, const void* bias,
+               const void* resid, void* aux, int accumulate, void* stream);
+
+/* LayerNorm forward over `rows` rows of width h (h % 8 == 0, h <= 8192):
+ * y = gamma * (x - mean) * rstd + beta; mean and rstd fp32 [rows]. */
+int merak_layernorm_fwd(int dtype, int rows, int h, float eps, const void* x, const void* gamma,
+                        const void* beta, void* y, float* mean, float* rstd, void* stream);
+
+/* fp32 scratch elements needed by the column reductions below for a
+ * [rows, cols] input (0 for empty input). */
+size_t merak_reduce_scratch_elems(int rows, int cols);
+
+/* LayerNorm backward fused with the residual-gradient add:
+ * dx = dres + LN'(dout).  dgamma = sum over rows of dout * xhat, dbeta = sum of
+ * dout, both written (accumulate = 0) or added (accumulate = 1), summed in a
+ * fixed order (deterministic).  scratch: fp32, 2 * merak_reduce_scratch_elems(rows, h). */
+int merak_layernorm_bwd(int dtype, int rows, int h, const void* dout, const void* x,
+                        const float* mean, const float* rstd, const void* gamma,
+                        const void* dres, void* dx, float* dgamma, float* dbeta,
+                        int accumulate, float* scratch, void* stream);
+
+/* out[c] (= or +=) sum over rows r of x[r, c] (fp32 out; cols % 8 == 0), fixed
+ * summation order.  scratch: fp32, merak_reduce_scratch_elems(rows, cols). */
+int merak_column_sum(int dtype, int rows, int cols, const void* x, float* out, int accumulate,
+                     float* scratch, void* stream);
+
+/* Causal attention forward on a packed qkv buffer [batch, seq, 3, heads, d]
+ * (row stride 3*heads*d, the QKV GEMM's output layout): o [batch, seq, heads, d]
+ * and lse fp32 [batch, heads, seq] = natural log of sum_j exp(q_i k_j / sqrt(d))
+ * over j <= i.  seq % 64 == 0; d in {64, 96, 128}. */
+int merak_attention_fwd(int dtype, int batch, int seq, int heads, int head_dim,
+                        const void* qkv, void* o, float* lse, void* stream);
+
+/* Causal attention backward: dqkv [batch, seq, 3, heads, d] from qkv, o, lse and
+ * dout [batch, seq, heads, d].  delta: fp32 scratch of batch*heads*seq elements.
+ * Deterministic (no atomics). */
+int merak_attention_bwd(int dtype, int batch, int seq, int heads, int head_dim,
+                        const void* qkv, const void* o, const float* lse, const void* dout,
+                        void* dqkv, float* delta, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MERAK_STAGE_H */

@@ -1,0 +1,702 @@
+// Stage runtime and C ABI (include/merak_stage.h).
+//
+// Host-side schedule of one GPU's share of a pipeline stage:
+//   * forward: for each block, the micro-batch's n sub-micro-batches (even,
+//     independent splits along the batch axis, paper Sec. 5.3) are issued on
+//     stream (j mod 2), so one slice's GEMMs can run beside another slice's
+//     LayerNorm/attention work;
+//   * blocks whose recompute bit is set keep only their input (paper Sec. 5.2);
+//     merak_stage_recompute rebuilds their activations from it and needs no
+//     upstream gradient (early recomputation, Sec. 5.1);
+//   * backward: per block, the sub-micro-batches' input-gradient chains run on
+//     the two streams; the block's weight, bias and LayerNorm gradients are
+//     then formed over the whole micro-batch on an internal third stream
+//     (parity-double-buffered scratch lets the next block's chains proceed
+//     meanwhile).  No floating-point atomics: results are deterministic.
+// The AllReduces of tensor parallelism are the identity on one GPU; their
+// inputs (partial sums) go to the caller's hand-off buffers.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <map>
+#include <mutex>
+#include <new>
+
+#include "../../include/merak_stage.h"
+#include "kernels.h"
+
+using namespace merak;
+
+namespace {
+
+constexpr int kMaxBlocks = 64;
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+struct Dims {
+  int L, h, a, f, s, b, t, n;
+  int hl, fl, al, d;
+  int T, Ms, bs;  // tokens per micro-batch, tokens and samples per sub-micro-batch
+  int dtype;
+  size_t esz;
+  uint64_t mask;
+  float eps;
+};
+
+int check_config(const merak_stage_config* c) {
+  if (!c) return MERAK_ERR_INVALID_ARG;
+  if (c->dtype != MERAK_BF16 && c->dtype != MERAK_FP32) return MERAK_ERR_INVALID_ARG;
+  if (c->n_blocks < 1 || c->n_blocks > kMaxBlocks) return MERAK_ERR_SHAPE;
+  if (c->hidden <= 0 || c->n_heads <= 0 || c->ffn <= 0 || c->seq_len <= 0 || c->micro_batch <= 0 ||
+      c->tp_degree <= 0 || c->n_sub_microbatches <= 0)
+    return MERAK_ERR_SHAPE;
+  if (c->n_heads % c->tp_degree != 0 || c->hidden % c->n_heads != 0 || c->ffn % c->tp_degree != 0 ||
+      c->micro_batch % c->n_sub_microbatches != 0)
+    return MERAK_ERR_SHAPE;
+  if (c->hidden % 64 != 0 || (c->hidden / c->tp_degree) % 64 != 0 || (c->ffn / c->tp_degree) % 64 != 0 ||
+      c->seq_len % 64 != 0)
+    return MERAK_ERR_SHAPE;
+  if (c->n_blocks < 64 && (c->recompute_mask >> c->n_blocks) != 0) return MERAK_ERR_SHAPE;
+  if (!(c->ln_eps > 0.0f)) return MERAK_ERR_SHAPE;
+  // Sizes must fit the 32-bit indexing of the launch interface.
+  const int64_t T = (int64_t)c->micro_batch * c->seq_len;
+  if (T * (int64_t)c->ffn / c->tp_degree >= ((int64_t)1 << 31) || T * (int64_t)c->hidden * 3 >= ((int64_t)1 << 31))
+    return MERAK_ERR_SHAPE;
+  const int d = c->hidden / c->n_heads;
+  if (d != 64 && d != 96 && d != 128) return MERAK_ERR_UNSUPPORTED;
+  return MERAK_OK;
+}
+
+Dims make_dims(const merak_stage_config* c) {
+  Dims D;
+  D.L = c->n_blocks; D.h = c->hidden; D.a = c->n_heads; D.f = c->ffn; D.s = c->seq_len; D.b = c->micro_batch;
+  D.t = c->tp_degree; D.n = c->n_sub_microbatches;
+  D.hl = D.h / D.t; D.fl = D.f / D.t; D.al = D.a / D.t; D.d = D.h / D.a;
+  D.T = D.b * D.s; D.bs = D.b / D.n; D.Ms = D.bs * D.s;
+  D.dtype = c->dtype;
+  D.esz = c->dtype == MERAK_BF16 ? 2 : 4;
+  D.mask = c->recompute_mask;
+  D.eps = c->ln_eps;
+  return D;
+}
+
+// Element offsets of the 12 tensors of one block, and the block stride.
+void block_param_offsets(const Dims& D, size_t off[MERAK_PARAMS_PER_BLOCK], size_t* stride) {
+  const size_t sizes[MERAK_PARAMS_PER_BLOCK] = {
+      (size_t)D.h, (size_t)D.h, (size_t)3 * D.hl * D.h, (size_t)3 * D.hl, (size_t)D.h * D.hl, (size_t)D.h,
+      (size_t)D.h, (size_t)D.h, (size_t)D.fl * D.h, (size_t)D.fl, (size_t)D.h * D.fl, (size_t)D.h};
+  size_t o = 0;
+  for (int i = 0; i < MERAK_PARAMS_PER_BLOCK; ++i) {
+    off[i] = o;
+    o = align_up(o + sizes[i], 64);
+  }
+  *stride = o;
+}
+
+enum { P_LN1G, P_LN1B, P_WQKV, P_BQKV, P_WO, P_BO, P_LN2G, P_LN2B, P_W1, P_B1, P_W2, P_B2 };
+
+// Byte offsets of one block's saved activations.
+struct ActLayout {
+  size_t ln1, mu1, rs1, qkv, o, lse, x1, ln2, mu2, rs2, u, g, size;
+};
+
+ActLayout act_layout(const Dims& D) {
+  ActLayout A;
+  size_t o = 0;
+  auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes, 256); return r; };
+  const size_t T = D.T, e = D.esz;
+  A.ln1 = take(T * D.h * e);
+  A.mu1 = take(T * 4);
+  A.rs1 = take(T * 4);
+  A.qkv = take(T * 3 * D.hl * e);
+  A.o = take(T * D.hl * e);
+  A.lse = take(T * D.al * 4);
+  A.x1 = take(T * D.h * e);
+  A.ln2 = take(T * D.h * e);
+  A.mu2 = take(T * 4);
+  A.rs2 = take(T * 4);
+  A.u = take(T * D.fl * e);
+  A.g = take(T * D.fl * e);
+  A.size = o;
+  return A;
+}
+
+// Backward scratch of one parity.
+struct BwdLayout {
+  size_t du, dln2, dx1, dO, dqkv, dln1, delta;
+  size_t p_bqkv, p_bo, p_b1, p_b2, p_g2, p_be2, p_g1, p_be1;
+  size_t size;
+};
+
+BwdLayout bwd_layout(const Dims& D) {
+  BwdLayout B;
+  size_t o = 0;
+  auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes, 256); return r; };
+  const size_t T = D.T, e = D.esz, G = reduce_groups(D.T);
+  B.du = take(T * D.fl * e);
+  B.dln2 = take(T * D.h * e);
+  B.dx1 = take(T * D.h * e);
+  B.dO = take(T * D.hl * e);
+  B.dqkv = take(T * 3 * D.hl * e);
+  B.dln1 = take(T * D.h * e);
+  B.delta = take(T * D.al * 4);
+  B.p_bqkv = take(G * 3 * D.hl * 4);
+  B.p_bo = take(G * D.h * 4);
+  B.p_b1 = take(G * D.fl * 4);
+  B.p_b2 = take(G * D.h * 4);
+  B.p_g2 = take(G * D.h * 4);
+  B.p_be2 = take(G * D.h * 4);
+  B.p_g1 = take(G * D.h * 4);
+  B.p_be1 = take(G * D.h * 4);
+  B.size = o;
+  return B;
+}
+
+struct WsLayout {
+  ActLayout act;
+  BwdLayout bwd;
+  size_t xs;          // (L-1) block-input checkpoints
+  size_t keep_acts;   // activations of non-recomputed blocks
+  size_t fwd_tmp;     // activations of recomputed blocks during the forward pass
+  size_t chain;       // 3 input-gradient buffers
+  size_t par[2];      // backward scratch per parity
+  size_t rc_y;        // recompute's (unused) block output
+  size_t total;
+  size_t recompute_total;
+  int keep_slot[kMaxBlocks];  // index among kept blocks, or -1
+  int rc_slot[kMaxBlocks];    // index among recomputed blocks, or -1
+  int n_keep, n_rc;
+};
+
+WsLayout ws_layout(const Dims& D) {
+  WsLayout W;
+  W.act = act_layout(D);
+  W.bwd = bwd_layout(D);
+  W.n_keep = W.n_rc = 0;
+  for (int l = 0; l < D.L; ++l) {
+    const bool rc = (D.mask >> l) & 1;
+    W.keep_slot[l] = rc ? -1 : W.n_keep++;
+    W.rc_slot[l] = rc ? W.n_rc++ : -1;
+  }
+  const size_t th = align_up((size_t)D.T * D.h * D.esz, 256);
+  size_t o = 0;
+  W.xs = o; o += (size_t)(D.L - 1) * th;
+  W.keep_acts = o; o += (size_t)W.n_keep * W.act.size;
+  W.fwd_tmp = o; o += (W.n_rc > 0 ? W.act.size : 0);
+  W.chain = o; o += 3 * th;
+  W.par[0] = o; o += W.bwd.size;
+  W.par[1] = o; o += W.bwd.size;
+  W.rc_y = o; o += (W.n_rc > 0 ? th : 0);
+  W.total = o;
+  W.recompute_total = (size_t)W.n_rc * W.act.size;
+  return W;
+}
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Handle
+// ---------------------------------------------------------------------------
+struct merak_stage {
+  merak_stage_config cfg;
+  Dims D;
+  WsLayout W;
+  size_t p_off[MERAK_PARAMS_PER_BLOCK];
+  size_t p_stride;
+  char* ws;
+  char* rc;
+  hipStream_t aux;
+  hipEvent_t ev_fork, ev_s1, ev_j0, ev_j1, ev_aux, ev_dw[2];
+  int state;  // 0 idle, 1 forward pending, 2 recomputed
+  const void* x0;
+};
+
+namespace {
+
+enum { ST_IDLE = 0, ST_FWD = 1, ST_RECOMPUTED = 2 };
+
+std::mutex g_mu;
+std::map<void*, merak_stage*> g_rc_owner;  // recompute area -> handle that last filled it
+
+char* block_input(merak_stage* S, int l) {
+  if (l == 0) return (char*)S->x0;
+  return S->ws + S->W.xs + (size_t)(l - 1) * align_up((size_t)S->D.T * S->D.h * S->D.esz, 256);
+}
+
+// Saved activations of block l: during the forward pass (phase 0) recomputed
+// blocks use the temporary set; after recompute (phase 1) they use their slot
+// in the recompute area.
+char* block_acts(merak_stage* S, int l, int phase) {
+  if (S->W.keep_slot[l] >= 0) return S->ws + S->W.keep_acts + (size_t)S->W.keep_slot[l] * S->W.act.size;
+  if (phase == 0) return S->ws + S->W.fwd_tmp;
+  return S->rc + (size_t)S->W.rc_slot[l] * S->W.act.size;
+}
+
+#define HIP_TRY(expr)                          \
+  do {                                         \
+    hipError_t e_ = (expr);                    \
+    if (e_ != hipSuccess) return MERAK_ERR_HIP; \
+  } while (0)
+
+inline const char* P(const void* params, const merak_stage* S, int l, int which) {
+  return (const char*)params + (S->p_stride * l + S->p_off[which]) * S->D.esz;
+}
+
+GemmProblem gp(int M, int N, int K, const void* a, int lda, const void* b, int ldb, void* c, int ldc,
+               const void* bias = nullptr, const void* resid = nullptr, void* aux = nullptr, int acc = 0) {
+  GemmProblem p;
+  p.M = M; p.N = N; p.K = K; p.a = a; p.lda = lda; p.b = b; p.ldb = ldb; p.c = c; p.ldc = ldc;
+  p.bias = bias; p.resid = resid; p.aux = aux; p.accumulate = acc;
+  return p;
+}
+
+// Forward of block l for sub-micro-batch j on stream st.
+int block_forward(merak_stage* S, const void* params, int l, int j, char* A, const char* x, char* y,
+                  char* part_o, char* part_f, hipStream_t st) {
+  const Dims& D = S->D;
+  const ActLayout& L = S->W.act;
+  const int dt = D.dtype;
+  const size_t r0 = (size_t)j * D.Ms;
+  const size_t e = D.esz;
+  const int M = D.Ms;
+  // LN1
+  HIP_TRY(launch_layernorm_fwd(dt, M, D.h, D.eps, x + r0 * D.h * e, P(params, S, l, P_LN1G), P(params, S, l, P_LN1B),
+                               A + L.ln1 + r0 * D.h * e, (float*)(A + L.mu1) + r0, (float*)(A + L.rs1) + r0, st));
+  // QKV (column parallel) + bias
+  GemmProblem p = gp(M, 3 * D.hl, D.h, A + L.ln1 + r0 * D.h * e, D.h, P(params, S, l, P_WQKV), D.h,
+                     A + L.qkv + r0 * 3 * D.hl * e, 3 * D.hl, P(params, S, l, P_BQKV));
+  HIP_TRY(launch_gemm(dt, false, false, EPI_BIAS, &p, 1, st));
+  // causal attention on the local heads
+  HIP_TRY(launch_attention_fwd(dt, D.bs, D.s, D.al, D.d, A + L.qkv + r0 * 3 * D.hl * e, A + L.o + r0 * D.hl * e,
+                               (float*)(A + L.lse) + (size_t)j * D.bs * D.al * D.s, st));
+  // projection (row parallel): partial sum -> hand-off; x1 = x + partial + b_o
+  p = gp(M, D.h, D.hl, A + L.o + r0 * D.hl * e, D.hl, P(params, S, l, P_WO), D.hl, A + L.x1 + r0 * D.h * e, D.h,
+         P(params, S, l, P_BO), x + r0 * D.h * e, part_o ? part_o + r0 * D.h * e : nullptr);
+  HIP_TRY(launch_gemm(dt, false, false, EPI_BIAS_RESID, &p, 1, st));
+  // LN2
+  HIP_TRY(launch_layernorm_fwd(dt, M, D.h, D.eps, A + L.x1 + r0 * D.h * e, P(params, S, l, P_LN2G),
+                               P(params, S, l, P_LN2B), A + L.ln2 + r0 * D.h * e, (float*)(A + L.mu2) + r0,
+                               (float*)(A + L.rs2) + r0, st));
+  // FC1 (column parallel) + bias + GeLU; keeps the pre-activation u
+  p = gp(M, D.fl, D.h, A + L.ln2 + r0 * D.h * e, D.h, P(params, S, l, P_W1), D.h, A + L.g + r0 * D.fl * e, D.fl,
+         P(params, S, l, P_B1), nullptr, A + L.u + r0 * D.fl * e);
+  HIP_TRY(launch_gemm(dt, false, false, EPI_BIAS_GELU, &p, 1, st));
+  // FC2 (row parallel): partial sum -> hand-off; y = x1 + partial + b2
+  p = gp(M, D.h, D.fl, A + L.g + r0 * D.fl * e, D.fl, P(params, S, l, P_W2), D.fl, y + r0 * D.h * e, D.h,
+         P(params, S, l, P_B2), A + L.x1 + r0 * D.h * e, part_f ? part_f + r0 * D.h * e : nullptr);
+  HIP_TRY(launch_gemm(dt, false, false, EPI_BIAS_RESID, &p, 1, st));
+  return MERAK_OK;
+}
+
+// Input-gradient chain of block l for sub-micro-batch j.
+int block_backward_chain(merak_stage* S, const void* params, int l, int j, const char* A, const char* x,
+                         const char* dy, char* dx, char* B, char* d_ln1, char* d_ln2, hipStream_t st) {
+  const Dims& D = S->D;
+  const ActLayout& L = S->W.act;
+  const BwdLayout& Bl = S->W.bwd;
+  const int dt = D.dtype;
+  const size_t r0 = (size_t)j * D.Ms;
+  const size_t e = D.esz;
+  const int M = D.Ms;
+  // FC2 backward: dg = dy W2; du = dg * gelu'(u)
+  GemmProblem p = gp(M, D.fl, D.h, dy + r0 * D.h * e, D.h, P(params, S, l, P_W2), D.fl, B + Bl.du + r0 * D.fl * e,
+                     D.fl, nullptr, nullptr, (void*)(A + L.u + r0 * D.fl * e));
+  HIP_TRY(launch_gemm(dt, false, true, EPI_GELU_BWD, &p, 1, st));
+  // FC1 backward: d_ln2 partial = du W1 (hand-off)
+  p = gp(M, D.h, D.fl, B + Bl.du + r0 * D.fl * e, D.fl, P(params, S, l, P_W1), D.h, d_ln2 + r0 * D.h * e, D.h);
+  HIP_TRY(launch_gemm(dt, false, true, EPI_STORE, &p, 1, st));
+  // LN2 backward + residual gradient: dx1 = dy + LN2'(d_ln2)
+  HIP_TRY(launch_layernorm_bwd(dt, M, D.h, d_ln2 + r0 * D.h * e, A + L.x1 + r0 * D.h * e,
+                               (const float*)(A + L.mu2) + r0, (const float*)(A + L.rs2) + r0,
+                               P(params, S, l, P_LN2G), dy + r0 * D.h * e, B + Bl.dx1 + r0 * D.h * e, st));
+  // projection backward: dO = dx1 W_o
+  p = gp(M, D.hl, D.h, B + Bl.dx1 + r0 * D.h * e, D.h, P(params, S, l, P_WO), D.hl, B + Bl.dO + r0 * D.hl * e, D.hl);
+  HIP_TRY(launch_gemm(dt, false, true, EPI_STORE, &p, 1, st));
+  // attention backward -> dqkv
+  const size_t lse_off = (size_t)j * D.bs * D.al * D.s;
+  HIP_TRY(launch_attention_bwd(dt, D.bs, D.s, D.al, D.d, A + L.qkv + r0 * 3 * D.hl * e, A + L.o + r0 * D.hl * e,
+                               (const float*)(A + L.lse) + lse_off, B + Bl.dO + r0 * D.hl * e,
+                               B + Bl.dqkv + r0 * 3 * D.hl * e, (float*)(B + Bl.delta) + lse_off, st));
+  // QKV backward: d_ln1 partial = dqkv W_qkv (hand-off)
+  p = gp(M, D.h, 3 * D.hl, B + Bl.dqkv + r0 * 3 * D.hl * e, 3 * D.hl, P(params, S, l, P_WQKV), D.h,
+         d_ln1 + r0 * D.h * e, D.h);
+  HIP_TRY(launch_gemm(dt, false, true, EPI_STORE, &p, 1, st));
+  // LN1 backward + residual gradient: dx = dx1 + LN1'(d_ln1)
+  HIP_TRY(launch_layernorm_bwd(dt, M, D.h, d_ln1 + r0 * D.h * e, x + r0 * D.h * e, (const float*)(A + L.mu1) + r0,
+                               (const float*)(A + L.rs1) + r0, P(params, S, l, P_LN1G), B + Bl.dx1 + r0 * D.h * e,
+                               dx + r0 * D.h * e, st));
+  return MERAK_OK;
+}
+
+// Weight, bias and LayerNorm gradients of block l over the whole micro-batch.
+int block_param_grads(merak_stage* S, int l, const char* A, const char* x, const char* dy, const char* B,
+                      const char* d_ln1, const char* d_ln2, float* grads, int acc, hipStream_t st) {
+  const Dims& D = S->D;
+  const ActLayout& L = S->W.act;
+  const BwdLayout& Bl = S->W.bwd;
+  const int dt = D.dtype;
+  const int T = D.T;
+  float* g = grads + S->p_stride * l;
+  // dW = dY^T X for the four linear layers, one grouped launch.
+  GemmProblem p[4];
+  p[0] = gp(3 * D.hl, D.h, T, B + Bl.dqkv, 3 * D.hl, A + L.ln1, D.h, g + S->p_off[P_WQKV], D.h, nullptr, nullptr,
+            nullptr, acc);
+  p[1] = gp(D.h, D.hl, T, B + Bl.dx1, D.h, A + L.o, D.hl, g + S->p_off[P_WO], D.hl, nullptr, nullptr, nullptr, acc);
+  p[2] = gp(D.fl, D.h, T, B + Bl.du, D.fl, A + L.ln2, D.h, g + S->p_off[P_W1], D.h, nullptr, nullptr, nullptr, acc);
+  p[3] = gp(D.h, D.fl, T, dy, D.h, A + L.g, D.fl, g + S->p_off[P_W2], D.fl, nullptr, nullptr, nullptr, acc);
+  HIP_TRY(launch_gemm(dt, true, true, EPI_F32, p, 4, st));
+  // bias gradients: token sums of the layer output gradients
+  const int G = (int)reduce_groups(T);
+  float* pb;
+  pb = (float*)(B + Bl.p_bqkv);
+  HIP_TRY(launch_column_partials(dt, T, 3 * D.hl, B + Bl.dqkv, pb, st));
+  HIP_TRY(launch_reduce_partials(G, 3 * D.hl, pb, g + S->p_off[P_BQKV], acc, st));
+  pb = (float*)(B + Bl.p_bo);
+  HIP_TRY(launch_column_partials(dt, T, D.h, B + Bl.dx1, pb, st));
+  HIP_TRY(launch_reduce_partials(G, D.h, pb, g + S->p_off[P_BO], acc, st));
+  pb = (float*)(B + Bl.p_b1);
+  HIP_TRY(launch_column_partials(dt, T, D.fl, B + Bl.du, pb, st));
+  HIP_TRY(launch_reduce_partials(G, D.fl, pb, g + S->p_off[P_B1], acc, st));
+  pb = (float*)(B + Bl.p_b2);
+  HIP_TRY(launch_column_partials(dt, T, D.h, dy, pb, st));
+  HIP_TRY(launch_reduce_partials(G, D.h, pb, g + S->p_off[P_B2], acc, st));
+  // LayerNorm parameters
+  float* pg = (float*)(B + Bl.p_g2);
+  float* pbe = (float*)(B + Bl.p_be2);
+  HIP_TRY(launch_layernorm_param_partials(dt, T, D.h, d_ln2, A + L.x1, (const float*)(A + L.mu2),
+                                          (const float*)(A + L.rs2), pg, pbe, st));
+  HIP_TRY(launch_reduce_partials(G, D.h, pg, g + S->p_off[P_LN2G], acc, st));
+  HIP_TRY(launch_reduce_partials(G, D.h, pbe, g + S->p_off[P_LN2B], acc, st));
+  pg = (float*)(B + Bl.p_g1);
+  pbe = (float*)(B + Bl.p_be1);
+  HIP_TRY(launch_layernorm_param_partials(dt, T, D.h, d_ln1, x, (const float*)(A + L.mu1), (const float*)(A + L.rs1),
+                                          pg, pbe, st));
+  HIP_TRY(launch_reduce_partials(G, D.h, pg, g + S->p_off[P_LN1G], acc, st));
+  HIP_TRY(launch_reduce_partials(G, D.h, pbe, g + S->p_off[P_LN1B], acc, st));
+  return MERAK_OK;
+}
+
+int fork(merak_stage* S, hipStream_t s0, hipStream_t s1) {
+  HIP_TRY(hipEventRecord(S->ev_fork, s0));
+  HIP_TRY(hipStreamWaitEvent(s1, S->ev_fork, 0));
+  return MERAK_OK;
+}
+
+int join(merak_stage* S, hipStream_t s0, hipStream_t s1) {
+  HIP_TRY(hipEventRecord(S->ev_s1, s1));
+  HIP_TRY(hipStreamWaitEvent(s0, S->ev_s1, 0));
+  return MERAK_OK;
+}
+
+int check_ptr(const void* p) {
+  if (!p) return MERAK_ERR_INVALID_ARG;
+  if (!aligned(p, 16)) return MERAK_ERR_ALIGN;
+  return MERAK_OK;
+}
+
+#define TRY(expr)               \
+  do {                          \
+    int r_ = (expr);            \
+    if (r_ != MERAK_OK) return r_; \
+  } while (0)
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// C ABI
+// ---------------------------------------------------------------------------
+extern "C" {
+
+const char* merak_status_str(int status) {
+  switch (status) {
+    case MERAK_OK: return "ok";
+    case MERAK_ERR_INVALID_ARG: return "invalid argument";
+    case MERAK_ERR_SHAPE: return "unsupported or inconsistent shape";
+    case MERAK_ERR_ORDER: return "call-order violation";
+    case MERAK_ERR_ALIGN: return "misaligned pointer";
+    case MERAK_ERR_WORKSPACE: return "workspace too small";
+    case MERAK_ERR_HIP: return "HIP runtime error";
+    case MERAK_ERR_UNSUPPORTED: return "unsupported configuration";
+    default: return "unknown status";
+  }
+}
+
+int merak_stage_validate(const merak_stage_config* cfg) { return check_config(cfg); }
+
+int merak_stage_param_layout(const merak_stage_config* cfg, size_t* total_elems, size_t* offsets) {
+  TRY(check_config(cfg));
+  if (!total_elems) return MERAK_ERR_INVALID_ARG;
+  const Dims D = make_dims(cfg);
+  size_t off[MERAK_PARAMS_PER_BLOCK], stride;
+  block_param_offsets(D, off, &stride);
+  *total_elems = stride * D.L;
+  if (offsets)
+    for (int l = 0; l < D.L; ++l)
+      for (int i = 0; i < MERAK_PARAMS_PER_BLOCK; ++i) offsets[l * MERAK_PARAMS_PER_BLOCK + i] = stride * l + off[i];
+  return MERAK_OK;
+}
+
+int merak_stage_workspace_bytes(const merak_stage_config* cfg, size_t* workspace_bytes, size_t* recompute_bytes) {
+  TRY(check_config(cfg));
+  const WsLayout W = ws_layout(make_dims(cfg));
+  if (workspace_bytes) *workspace_bytes = W.total;
+  if (recompute_bytes) *recompute_bytes = W.recompute_total;
+  return MERAK_OK;
+}
+
+int merak_stage_create(const merak_stage_config* cfg, void* workspace, size_t workspace_bytes, void* recompute_area,
+                       size_t recompute_bytes, merak_stage_t* out) {
+  if (!out) return MERAK_ERR_INVALID_ARG;
+  *out = nullptr;
+  TRY(check_config(cfg));
+  const Dims D = make_dims(cfg);
+  const WsLayout W = ws_layout(D);
+  if (!workspace) return MERAK_ERR_INVALID_ARG;
+  if (!aligned(workspace, 256)) return MERAK_ERR_ALIGN;
+  if (workspace_bytes < W.total) return MERAK_ERR_WORKSPACE;
+  if (W.recompute_total > 0) {
+    if (!recompute_area) return MERAK_ERR_INVALID_ARG;
+    if (!aligned(recompute_area, 256)) return MERAK_ERR_ALIGN;
+    if (recompute_bytes < W.recompute_total) return MERAK_ERR_WORKSPACE;
+  }
+  merak_stage* S = new (std::nothrow) merak_stage();
+  if (!S) return MERAK_ERR_INVALID_ARG;
+  S->cfg = *cfg;
+  S->D = D;
+  S->W = W;
+  block_param_offsets(D, S->p_off, &S->p_stride);
+  S->ws = (char*)workspace;
+  S->rc = (char*)recompute_area;
+  S->state = ST_IDLE;
+  S->x0 = nullptr;
+  hipError_t e = hipStreamCreateWithFlags(&S->aux, hipStreamNonBlocking);
+  const bool have_stream = (e == hipSuccess);
+  hipEvent_t* evs[] = {&S->ev_fork, &S->ev_s1, &S->ev_j0, &S->ev_j1, &S->ev_aux, &S->ev_dw[0], &S->ev_dw[1]};
+  int made = 0;
+  for (hipEvent_t* ev : evs) {
+    if (e != hipSuccess) break;
+    e = hipEventCreateWithFlags(ev, hipEventDisableTiming);
+    if (e == hipSuccess) ++made;
+  }
+  if (e != hipSuccess) {
+    for (int i = 0; i < made; ++i) (void)hipEventDestroy(*evs[i]);
+    if (have_stream) (void)hipStreamDestroy(S->aux);
+    delete S;
+    return MERAK_ERR_HIP;
+  }
+  *out = S;
+  return MERAK_OK;
+}
+
+int merak_stage_destroy(merak_stage_t S) {
+  if (!S) return MERAK_ERR_INVALID_ARG;
+  {
+    std::lock_guard<std::mutex> lk(g_mu);
+    for (auto it = g_rc_owner.begin(); it != g_rc_owner.end();)
+      it = (it->second == S) ? g_rc_owner.erase(it) : std::next(it);
+  }
+  hipEvent_t evs[] = {S->ev_fork, S->ev_s1, S->ev_j0, S->ev_j1, S->ev_aux, S->ev_dw[0], S->ev_dw[1]};
+  for (hipEvent_t ev : evs) (void)hipEventDestroy(ev);
+  (void)hipStreamDestroy(S->aux);
+  delete S;
+  return MERAK_OK;
+}
+
+int merak_stage_fwd(merak_stage_t S, const void* params, const void* x, void* y, void* fwd_partials, void* stream0,
+                    void* stream1) {
+  if (!S) return MERAK_ERR_INVALID_ARG;
+  TRY(check_ptr(params));
+  TRY(check_ptr(x));
+  TRY(check_ptr(y));
+  if (fwd_partials && !aligned(fwd_partials, 16)) return MERAK_ERR_ALIGN;
+  hipStream_t s0 = (hipStream_t)stream0, s1 = (hipStream_t)stream1;
+  const Dims& D = S->D;
+  S->x0 = x;
+  S->state = ST_FWD;
+  TRY(fork(S, s0, s1));
+  const size_t th = (size_t)D.T * D.h * D.esz;
+  for (int l = 0; l < D.L; ++l) {
+    char* A = block_acts(S, l, 0);
+    const char* xin = block_input(S, l);
+    char* yout = (l == D.L - 1) ? (char*)y : block_input(S, l + 1);
+    char* po = fwd_partials ? (char*)fwd_partials + (size_t)(2 * l) * th : nullptr;
+    char* pf = fwd_partials ? (char*)fwd_partials + (size_t)(2 * l + 1) * th : nullptr;
+    for (int j = 0; j < D.n; ++j)
+      TRY(block_forward(S, params, l, j, A, xin, yout, po, pf, (j & 1) ? s1 : s0));
+  }
+  TRY(join(S, s0, s1));
+  return MERAK_OK;
+}
+
+int merak_stage_recompute(merak_stage_t S, const void* params, void* stream0, void* stream1) {
+  if (!S) return MERAK_ERR_INVALID_ARG;
+  TRY(check_ptr(params));
+  if (S->state == ST_IDLE) return MERAK_ERR_ORDER;
+  if (S->D.mask == 0) return MERAK_OK;
+  hipStream_t s0 = (hipStream_t)stream0, s1 = (hipStream_t)stream1;
+  const Dims& D = S->D;
+  TRY(fork(S, s0, s1));
+  for (int l = 0; l < D.L; ++l) {
+    if (!((D.mask >> l) & 1)) continue;
+    char* A = block_acts(S, l, 1);
+    const char* xin = block_input(S, l);
+    char* yout = S->ws + S->W.rc_y;  // the block output is already checkpointed
+    for (int j = 0; j < D.n; ++j)
+      TRY(block_forward(S, params, l, j, A, xin, yout, nullptr, nullptr, (j & 1) ? s1 : s0));
+  }
+  TRY(join(S, s0, s1));
+  {
+    std::lock_guard<std::mutex> lk(g_mu);
+    g_rc_owner[S->rc] = S;
+  }
+  S->state = ST_RECOMPUTED;
+  return MERAK_OK;
+}
+
+int merak_stage_bwd(merak_stage_t S, const void* params, const void* dy, void* dx, float* grads, int accumulate,
+                    void* bwd_partials, void* stream0, void* stream1) {
+  if (!S) return MERAK_ERR_INVALID_ARG;
+  TRY(check_ptr(params));
+  TRY(check_ptr(dy));
+  TRY(check_ptr(dx));
+  TRY(check_ptr(grads));
+  if (accumulate != 0 && accumulate != 1) return MERAK_ERR_INVALID_ARG;
+  if (bwd_partials && !aligned(bwd_partials, 16)) return MERAK_ERR_ALIGN;
+  if (S->state == ST_IDLE) return MERAK_ERR_ORDER;
+  if (S->D.mask != 0) {
+    if (S->state != ST_RECOMPUTED) return MERAK_ERR_ORDER;
+    std::lock_guard<std::mutex> lk(g_mu);
+    auto it = g_rc_owner.find(S->rc);
+    if (it == g_rc_owner.end() || it->second != S) return MERAK_ERR_ORDER;
+  }
+  hipStream_t s0 = (hipStream_t)stream0, s1 = (hipStream_t)stream1;
+  const Dims& D = S->D;
+  const size_t th = (size_t)D.T * D.h * D.esz;
+  const size_t th_al = align_up(th, 256);
+  TRY(fork(S, s0, s1));
+  HIP_TRY(hipStreamWaitEvent(S->aux, S->ev_fork, 0));
+  for (int l = D.L - 1; l >= 0; --l) {
+    const int par = l & 1;
+    char* A = block_acts(S, l, 1);
+    const char* xin = block_input(S, l);
+    const char* dyl = (l == D.L - 1) ? (const char*)dy : S->ws + S->W.chain + (size_t)((l + 1) % 3) * th_al;
+    char* dxl = (l == 0) ? (char*)dx : S->ws + S->W.chain + (size_t)(l % 3) * th_al;
+    char* B = S->ws + S->W.par[par];
+    char* d1 = bwd_partials ? (char*)bwd_partials + (size_t)(2 * l) * th : B + S->W.bwd.dln1;
+    char* d2 = bwd_partials ? (char*)bwd_partials + (size_t)(2 * l + 1) * th : B + S->W.bwd.dln2;
+    if (l <= D.L - 3) {  // parity scratch was last read by the gradients of block l+2
+      HIP_TRY(hipStreamWaitEvent(s0, S->ev_dw[par], 0));
+      HIP_TRY(hipStreamWaitEvent(s1, S->ev_dw[par], 0));
+    }
+    for (int j = 0; j < D.n; ++j)
+      TRY(block_backward_chain(S, params, l, j, A, xin, dyl, dxl, B, d1, d2, (j & 1) ? s1 : s0));
+    HIP_TRY(hipEventRecord(S->ev_j0, s0));
+    HIP_TRY(hipEventRecord(S->ev_j1, s1));
+    HIP_TRY(hipStreamWaitEvent(S->aux, S->ev_j0, 0));
+    HIP_TRY(hipStreamWaitEvent(S->aux, S->ev_j1, 0));
+    TRY(block_param_grads(S, l, A, xin, dyl, B, d1, d2, grads, accumulate, S->aux));
+    HIP_TRY(hipEventRecord(S->ev_dw[par], S->aux));
+  }
+  HIP_TRY(hipEventRecord(S->ev_aux, S->aux));
+  TRY(join(S, s0, s1));
+  HIP_TRY(hipStreamWaitEvent(s0, S->ev_aux, 0));
+  S->state = ST_IDLE;
+  return MERAK_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Per-kernel entry points
+// ---------------------------------------------------------------------------
+int merak_gemm(int dtype, int a_trans, int b_trans, int epilogue, int M, int N, int K, const void* a, int lda,
+               const void* b, int ldb, void* c, const void* bias, const void* resid, void* aux, int accumulate,
+               void* stream) {
+  if (dtype != MERAK_BF16 && dtype != MERAK_FP32) return MERAK_ERR_INVALID_ARG;
+  if ((a_trans != 0 && a_trans != 1) || (b_trans != 0 && b_trans != 1)) return MERAK_ERR_INVALID_ARG;
+  if (epilogue < 0 || epilogue >= EPI_COUNT) return MERAK_ERR_INVALID_ARG;
+  if (M <= 0 || N <= 0 || K <= 0 || M % 64 || N % 64 || K % 64) return MERAK_ERR_SHAPE;
+  if (lda < (a_trans ? M : K) || ldb < (b_trans ? N : K) || lda % 8 || ldb % 8) return MERAK_ERR_SHAPE;
+  TRY(check_ptr(a));
+  TRY(check_ptr(b));
+  TRY(check_ptr(c));
+  const bool need_bias = epilogue == EPI_BIAS || epilogue == EPI_BIAS_GELU || epilogue == EPI_BIAS_RESID;
+  if (need_bias) TRY(check_ptr(bias));
+  if (epilogue == EPI_BIAS_RESID) TRY(check_ptr(resid));
+  if (epilogue == EPI_BIAS_GELU || epilogue == EPI_GELU_BWD) TRY(check_ptr(aux));
+  if (aux && !aligned(aux, 16)) return MERAK_ERR_ALIGN;
+  if (accumulate != 0 && accumulate != 1) return MERAK_ERR_INVALID_ARG;
+  GemmProblem p = gp(M, N, K, a, lda, b, ldb, c, N, bias, resid, aux, accumulate);
+  HIP_TRY(launch_gemm(dtype, a_trans, b_trans, epilogue, &p, 1, (hipStream_t)stream));
+  return MERAK_OK;
+}
+
+int merak_layernorm_fwd(int dtype, int rows, int h, float eps, const void* x, const void* gamma, const void* beta,
+                        void* y, float* mean, float* rstd, void* stream) {
+  if (dtype != MERAK_BF16 && dtype != MERAK_FP32) return MERAK_ERR_INVALID_ARG;
+  if (rows <= 0 || h <= 0 || h % 8 || h > 8192 || !(eps > 0.0f)) return MERAK_ERR_SHAPE;
+  TRY(check_ptr(x)); TRY(check_ptr(gamma)); TRY(check_ptr(beta)); TRY(check_ptr(y));
+  TRY(check_ptr(mean)); TRY(check_ptr(rstd));
+  HIP_TRY(launch_layernorm_fwd(dtype, rows, h, eps, x, gamma, beta, y, mean, rstd, (hipStream_t)stream));
+  return MERAK_OK;
+}
+
+size_t merak_reduce_scratch_elems(int rows, int cols) {
+  if (rows <= 0 || cols <= 0) return 0;
+  return reduce_groups(rows) * (size_t)cols;
+}
+
+int merak_layernorm_bwd(int dtype, int rows, int h, const void* dout, const void* x, const float* mean,
+                        const float* rstd, const void* gamma, const void* dres, void* dx, float* dgamma,
+                        float* dbeta, int accumulate, float* scratch, void* stream) {
+  if (dtype != MERAK_BF16 && dtype != MERAK_FP32) return MERAK_ERR_INVALID_ARG;
+  if (rows <= 0 || h <= 0 || h % 8 || h > 8192) return MERAK_ERR_SHAPE;
+  if (accumulate != 0 && accumulate != 1) return MERAK_ERR_INVALID_ARG;
+  TRY(check_ptr(dout)); TRY(check_ptr(x)); TRY(check_ptr(mean)); TRY(check_ptr(rstd)); TRY(check_ptr(gamma));
+  TRY(check_ptr(dres)); TRY(check_ptr(dx)); TRY(check_ptr(dgamma)); TRY(check_ptr(dbeta)); TRY(check_ptr(scratch));
+  hipStream_t st = (hipStream_t)stream;
+  const size_t n = merak_reduce_scratch_elems(rows, h);
+  const int G = (int)reduce_groups(rows);
+  HIP_TRY(launch_layernorm_bwd(dtype, rows, h, dout, x, mean, rstd, gamma, dres, dx, st));
+  HIP_TRY(launch_layernorm_param_partials(dtype, rows, h, dout, x, mean, rstd, scratch, scratch + n, st));
+  HIP_TRY(launch_reduce_partials(G, h, scratch, dgamma, accumulate, st));
+  HIP_TRY(launch_reduce_partials(G, h, scratch + n, dbeta, accumulate, st));
+  return MERAK_OK;
+}
+
+int merak_column_sum(int dtype, int rows, int cols, const void* x, float* out, int accumulate, float* scratch,
+                     void* stream) {
+  if (dtype != MERAK_BF16 && dtype != MERAK_FP32) return MERAK_ERR_INVALID_ARG;
+  if (rows <= 0 || cols <= 0 || cols % 8) return MERAK_ERR_SHAPE;
+  if (accumulate != 0 && accumulate != 1) return MERAK_ERR_INVALID_ARG;
+  TRY(check_ptr(x)); TRY(check_ptr(out)); TRY(check_ptr(scratch));
+  hipStream_t st = (hipStream_t)stream;
+  HIP_TRY(launch_column_partials(dtype, rows, cols, x, scratch, st));
+  HIP_TRY(launch_reduce_partials((int)reduce_groups(rows), cols, scratch, out, accumulate, st));
+  return MERAK_OK;
+}
+
+int merak_attention_fwd(int dtype, int batch, int seq, int heads, int head_dim, const void* qkv, void* o, float* lse,
+                        void* stream) {
+  if (dtype != MERAK_BF16 && dtype != MERAK_FP32) return MERAK_ERR_INVALID_ARG;
+  if (batch <= 0 || heads <= 0 || seq <= 0 || seq % 64) return MERAK_ERR_SHAPE;
+  if (head_dim != 64 && head_dim != 96 && head_dim != 128) return MERAK_ERR_UNSUPPORTED;
+  TRY(check_ptr(qkv)); TRY(check_ptr(o)); TRY(check_ptr(lse));
+  HIP_TRY(launch_attention_fwd(dtype, batch, seq, heads, head_dim, qkv, o, lse, (hipStream_t)stream));
+  return MERAK_OK;
+}
+
+int merak_attention_bwd(int dtype, int batch, int seq, int heads, int head_dim, const void* qkv, const void* o,
+                        const float* lse, const void* dout, void* dqkv, float* delta, void* stream) {
+  if (dtype != MERAK_BF16 && dtype != MERAK_FP32) return MERAK_ERR_INVALID_ARG;
+  if (batch <= 0 || heads <= 0 || seq <= 0 || seq % 64) return MERAK_ERR_SHAPE;
+  if (head_dim != 64 && head_dim != 96 && head_dim != 128) return MERAK_ERR_UNSUPPORTED;
+  TRY(check_ptr(qkv)); TRY(check_ptr(o)); TRY(check_ptr(lse)); TRY(check_ptr(dout)); TRY(check_ptr(dqkv));
+  TRY(check_ptr(delta));
+  HIP_TRY(launch_attention_bwd(dtype, batch, seq, heads, head_dim, qkv, o, lse, dout, dqkv, delta,
+                               (hipStream_t)stream));
+  return MERAK_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,117 @@
+"""Helpers for the GPU parity tests: run the HIP stage through the C ABI and the
+oracle on the same seeded inputs, and compare with the max-relative metric."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2206_04959_amd import binding as B
+from paper_2206_04959_amd import synth
+
+
+def need_gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.lib()  # raises if the HIP library is missing: no silent fallback
+    return torch
+
+
+def rel_err(got, ref) -> float:
+    ref = np.asarray(ref, dtype=np.float64)
+    got = np.asarray(got, dtype=np.float64)
+    den = float(np.max(np.abs(ref)))
+    return float(np.max(np.abs(got - ref))) / (den if den > 0 else 1.0)
+
+
+def tol_for(shape) -> float:
+    # stated tolerances: 2e-2 for bf16, 1e-4 for the fp32 check mode
+    return 2e-2 if shape.dtype == "bf16" else 1e-4
+
+
+class StageRun:
+    """Inputs on the device plus the outputs of one fwd -> recompute -> bwd call sequence."""
+
+    def __init__(self, shape, streams=2, with_partials=True, stage=None):
+        torch = need_gpu()
+        self.shape = shape
+        self.cfg = B.make_config(shape)
+        self.params_host = synth.stage_params(shape)
+        self.x_host = synth.stage_input(shape)
+        self.dy_host = synth.upstream_grad(shape)
+        flat = B.pack_params(self.cfg, [{k: v.payload for k, v in p.items()} for p in self.params_host])
+        self.params = B.to_device(flat)
+        self.x = B.to_device(self.x_host.payload)
+        self.dy = B.to_device(self.dy_host.payload)
+        dt = self.x.dtype
+        L, T, h = shape.n_blocks, shape.tokens, shape.hidden
+        self.y = torch.empty_like(self.x)
+        self.dx = torch.empty_like(self.x)
+        total, _ = B.param_layout(self.cfg)
+        self.grads = torch.full((total,), float("nan"), dtype=torch.float32, device="cuda")
+        self.fp = torch.empty((L, 2, T * h), dtype=dt, device="cuda") if with_partials else None
+        self.bp = torch.empty((L, 2, T * h), dtype=dt, device="cuda") if with_partials else None
+        self.stage = stage or B.Stage(shape)
+        if streams == 2:
+            self.streams = (torch.cuda.Stream(), torch.cuda.Stream())
+        else:
+            s = torch.cuda.Stream()
+            self.streams = (s, s)
+        self.torch = torch
+
+    def run(self, accumulate=False):
+        torch = self.torch
+        s0 = self.streams[0]
+        s0.wait_stream(torch.cuda.current_stream())
+        self.stage.fwd(self.params, self.x, self.y, self.fp, streams=self.streams)
+        self.stage.recompute(self.params, streams=self.streams)
+        self.stage.bwd(self.params, self.dy, self.dx, self.grads, accumulate, self.bp, streams=self.streams)
+        torch.cuda.current_stream().wait_stream(s0)
+        torch.cuda.synchronize()
+        return self
+
+    def results(self):
+        sh = self.shape
+        L = sh.n_blocks
+        out = dict(y=B.to_host_f64(self.y), dx=B.to_host_f64(self.dx))
+        g = self.grads.cpu().numpy().astype(np.float64)
+        out["grads"] = B.unpack(self.cfg, g, sh)
+        if self.fp is not None:
+            fp = B.to_host_f64(self.fp).reshape(L, 2, sh.micro_batch, sh.seq_len, sh.hidden)
+            bp = B.to_host_f64(self.bp).reshape(L, 2, sh.micro_batch, sh.seq_len, sh.hidden)
+            out["p_o"] = [fp[l, 0] for l in range(L)]
+            out["p_f"] = [fp[l, 1] for l in range(L)]
+            out["d_ln1"] = [bp[l, 0] for l in range(L)]
+            out["d_ln2"] = [bp[l, 1] for l in range(L)]
+        return out
+
+    def raw(self):
+        """Bit patterns of every output (for bit-equality checks)."""
+        torch = self.torch
+        r = dict(y=self.y.view(torch.int16).cpu().numpy() if self.y.dtype == torch.bfloat16 else self.y.cpu().numpy(),
+                 dx=self.dx.view(torch.int16).cpu().numpy() if self.dx.dtype == torch.bfloat16 else self.dx.cpu().numpy(),
+                 grads=self.grads.cpu().numpy().view(np.int32))
+        if self.fp is not None:
+            r["fp"] = self.fp.view(torch.int16).cpu().numpy() if self.fp.dtype == torch.bfloat16 else self.fp.cpu().numpy()
+            r["bp"] = self.bp.view(torch.int16).cpu().numpy() if self.bp.dtype == torch.bfloat16 else self.bp.cpu().numpy()
+        return r
+
+
+def oracle_results(shape):
+    params = [{k: v.f64 for k, v in p.items()} for p in synth.stage_params(shape)]
+    x = synth.stage_input(shape).f64
+    dy = synth.upstream_grad(shape).f64
+    return oracle.shard_run(x, dy, params, shape.local_heads, shape.ln_eps)
+
+
+def compare(got, ref, shape, tol=None, blocks=None):
+    """Return {tensor name: error}; every error must be <= tol."""
+    tol = tol_for(shape) if tol is None else tol
+    errs = {"y": rel_err(got["y"], ref["y"]), "dx": rel_err(got["dx"], ref["dx"])}
+    for l in (range(shape.n_blocks) if blocks is None else blocks):
+        if "p_o" in got:
+            for k in ("p_o", "p_f", "d_ln1", "d_ln2"):
+                errs[f"{k}[{l}]"] = rel_err(got[k][l], ref[k][l])
+        for name in synth.PARAM_NAMES:
+            errs[f"{name}[{l}]"] = rel_err(got["grads"][l][name], ref["grads"][l][name])
+    bad = {k: v for k, v in errs.items() if not (v <= tol)}
+    return errs, bad

@@ -1,0 +1,111 @@
+"""Whole-stage parity of the HIP path against the fp64 oracle, through the C ABI,
+plus the schedule properties the method guarantees (split independence,
+recomputation equality, determinism) and call-order errors."""
+import numpy as np
+import pytest
+
+from paper_2206_04959_amd import binding as B
+from paper_2206_04959_amd import synth
+from tests.gpu_util import StageRun, compare, need_gpu, oracle_results
+
+pytestmark = pytest.mark.gpu
+
+# Small shapes that still span several GEMM tiles, attention tiles and a ragged
+# 128-tile edge (3h/t = 384, h = 320 ...), each head_dim, tensor parallel shards.
+SMALL = {
+    "tiny-fp32": synth.TINY,
+    "tiny-bf16": synth.TINY.replace(dtype="bf16"),
+    "tiny-fp32-n2-rc": synth.TINY.replace(n_sub=2, recompute_mask=1),
+    "d64-t2-bf16": synth.StageShape("d64", n_blocks=3, hidden=512, n_heads=8, ffn=2048, seq_len=256,
+                                    micro_batch=4, tp_degree=2, n_sub=2, recompute_mask=0b010, seed=31),
+    "d96-bf16": synth.StageShape("d96", n_blocks=2, hidden=384, n_heads=4, ffn=1536, seq_len=192,
+                                 micro_batch=2, tp_degree=1, n_sub=2, recompute_mask=0b01, seed=32),
+    "d96-fp32": synth.StageShape("d96f", n_blocks=2, hidden=384, n_heads=4, ffn=1536, seq_len=128,
+                                 micro_batch=2, tp_degree=1, n_sub=2, recompute_mask=0b10, dtype="fp32",
+                                 x_std=1.0, seed=33),
+    "d128-t4-bf16": synth.StageShape("d128", n_blocks=2, hidden=1024, n_heads=8, ffn=4096, seq_len=128,
+                                     micro_batch=4, tp_degree=4, n_sub=4, recompute_mask=0b11, seed=34),
+}
+
+
+@pytest.mark.parametrize("name", sorted(SMALL))
+def test_stage_matches_oracle(name):
+    shape = SMALL[name]
+    print(f"[stage parity] {name}: {shape}", flush=True)
+    got = StageRun(shape).run().results()
+    ref = oracle_results(shape)
+    errs, bad = compare(got, ref, shape)
+    worst = max(errs, key=errs.get)
+    print(f"  worst {worst} = {errs[worst]:.3e}", flush=True)
+    assert not bad, bad
+
+
+def test_recompute_gives_bit_identical_gradients():
+    base = SMALL["d64-t2-bf16"]
+    a = StageRun(base.replace(recompute_mask=0)).run().raw()
+    b = StageRun(base.replace(recompute_mask=0b111)).run().raw()
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
+
+
+def test_sub_micro_batch_split_and_streams_do_not_change_results():
+    base = SMALL["d64-t2-bf16"]
+    ref = StageRun(base.replace(n_sub=1), streams=1).run().raw()
+    for n, streams in ((2, 2), (4, 2), (4, 1)):
+        got = StageRun(base.replace(n_sub=n), streams=streams).run().raw()
+        for k in ref:
+            assert np.array_equal(ref[k], got[k]), (n, streams, k)
+
+
+def test_runs_are_deterministic_and_accumulate_adds():
+    torch = need_gpu()
+    shape = SMALL["d96-bf16"]
+    r = StageRun(shape)
+    a = r.run().raw()
+    b = r.run().raw()
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
+    g1 = r.grads.clone()
+    r.run(accumulate=True)
+    assert torch.equal(r.grads, g1 + g1) or torch.allclose(r.grads, 2 * g1, rtol=1e-6, atol=0)
+
+
+def test_without_hand_off_buffers():
+    shape = SMALL["d96-bf16"]
+    ref = StageRun(shape).run().raw()
+    got = StageRun(shape, with_partials=False).run().raw()
+    for k in ("y", "dx", "grads"):
+        assert np.array_equal(ref[k], got[k]), k
+
+
+def test_call_order_errors():
+    torch = need_gpu()
+    shape = SMALL["tiny-fp32-n2-rc"]
+    r = StageRun(shape)
+    st = r.stage
+    with pytest.raises(B.MerakError) as e:
+        st.bwd(r.params, r.dy, r.dx, r.grads)
+    assert e.value.status == -3
+    with pytest.raises(B.MerakError) as e:
+        st.recompute(r.params)
+    assert e.value.status == -3
+    st.fwd(r.params, r.x, r.y)
+    with pytest.raises(B.MerakError) as e:  # recompute pending
+        st.bwd(r.params, r.dy, r.dx, r.grads)
+    assert e.value.status == -3
+    st.recompute(r.params)
+    # a second handle sharing the recompute area takes it over
+    other = B.Stage(shape, recompute_area=st.recompute_area)
+    other.fwd(r.params, r.x, r.y)
+    other.recompute(r.params)
+    with pytest.raises(B.MerakError) as e:
+        st.bwd(r.params, r.dy, r.dx, r.grads)
+    assert e.value.status == -3
+    other.bwd(r.params, r.dy, r.dx, r.grads)
+    st.recompute(r.params)
+    st.bwd(r.params, r.dy, r.dx, r.grads)
+    torch.cuda.synchronize()
+    with pytest.raises(B.MerakError) as e:  # consumed
+        st.bwd(r.params, r.dy, r.dx, r.grads)
+    assert e.value.status == -3
+    other.close()
