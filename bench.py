@@ -1,0 +1,202 @@
+#!/usr/bin/env python3
+"""Stage-shard benchmark on one MI355X.
+
+One step = forward + recompute + backward of one GPU's share of a GPT pipeline
+stage for one micro-batch (every step of the hot path), run through the C ABI
+of the HIP library on two streams.  Default workload: the 8.3B-shaped shard at
+tensor-parallel degree 4 (6 blocks, hidden 3072, 32 heads / 8 local, FFN 12288
+/ 3072 local, seq 1024, micro-batch 8 in 4 sub-micro-batches, recompute on 3
+of 6 blocks, bf16).  Inputs are seeded synthetic tensors already resident in
+HBM when timing starts.
+
+Prints one JSON line (last line of stdout).
+
+    python bench.py [--steps K] [--warmup W] [--config NAME] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2206_04959_amd import flops, synth  # noqa: E402
+
+METRIC = "stage-shard fwd+bwd TFLOP/s per MI355X and % bf16 MFMA peak (8.3B-shaped, t=4)"
+PEAK_BF16_TFLOPS = 2516.6   # dense bf16 MFMA: 256 CUs x 4096 FLOP/clk x 2.4 GHz
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_dw_traffic.json")
+GEMM_SOURCE = os.path.join(ROOT, "paper_2206_04959_amd", "csrc", "gemm.hip")
+
+
+def log(msg: str) -> None:
+    print(msg, file=sys.stderr, flush=True)
+
+
+def describe(s: synth.StageShape) -> str:
+    return (f"{s.name} stage shard: {s.n_blocks} blocks, hidden {s.hidden}, {s.n_heads} heads "
+            f"({s.local_heads} local, head_dim {s.head_dim}), ffn {s.ffn} ({s.local_ffn} local), seq {s.seq_len}, "
+            f"micro-batch {s.micro_batch} in {s.n_sub} sub-micro-batches, tp_degree {s.tp_degree}, "
+            f"recompute mask {bin(s.recompute_mask)}, {s.dtype}")
+
+
+def dw_traffic_bytes():
+    """HBM bytes per launch of the grouped weight-gradient GEMM, from the committed
+    rocprofv3 counter summary, or None if absent or taken on another kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+        src = hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()
+        if t.get("gemm_source_sha256") != src:
+            return None
+        return float(t["bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(shape: synth.StageShape, budget_s: float = 20.0):
+    """The fp64 oracle on a bounded sample of the same workload: one block of the
+    shard, one sequence, forward + backward, repeated while under budget."""
+    import numpy as np  # noqa: F401
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    sample = shape.replace(n_blocks=1, micro_batch=1, n_sub=1, recompute_mask=0, dtype="bf16")
+    params = [{k: v.f64 for k, v in p.items()} for p in synth.stage_params(sample)]
+    x = synth.stage_input(sample).f64
+    dy = synth.upstream_grad(sample).f64
+    reps, elapsed = 0, 0.0
+    while reps == 0 or (elapsed < budget_s / 2 and reps < 8):
+        t0 = time.perf_counter()
+        oracle.shard_run(x, dy, params, sample.local_heads, sample.ln_eps)
+        elapsed += time.perf_counter() - t0
+        reps += 1
+    work = flops.model_flops(sample) * reps
+    return {"value": work / elapsed / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": (f"fp64 NumPy oracle, forward+backward of 1 block x 1 sequence of the {shape.name} shard "
+                       f"({flops.model_flops(sample) / 1e9:.1f} GFLOP), {reps} run(s) in {elapsed:.1f} s")}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="gpt-8.3b-tp4", choices=sorted(synth.PRESETS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU's stage shard; --gpus {args.gpus} is not supported "
+              "(the cross-GPU reductions are replaced by hand-off buffers on one GPU).", file=sys.stderr)
+        return 2
+
+    import torch
+    from paper_2206_04959_amd import binding as B
+
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        return 1
+    shape = synth.PRESETS[args.config]
+    log(f"[bench] {describe(shape)}")
+    cfg = B.make_config(shape)
+    params = B.to_device(B.pack_params(cfg, [{k: v.payload for k, v in p.items()}
+                                              for p in synth.stage_params(shape)]))
+    x = B.to_device(synth.stage_input(shape).payload)
+    dy = B.to_device(synth.upstream_grad(shape).payload)
+    y = torch.empty_like(x)
+    dx = torch.empty_like(x)
+    total, _ = B.param_layout(cfg)
+    grads = torch.zeros(total, dtype=torch.float32, device="cuda")
+    L, T, h = shape.n_blocks, shape.tokens, shape.hidden
+    fwd_part = torch.empty((L, 2, T * h), dtype=x.dtype, device="cuda")
+    bwd_part = torch.empty((L, 2, T * h), dtype=x.dtype, device="cuda")
+    stage = B.Stage(shape)
+    log(f"[bench] workspace {stage.workspace_bytes / 2**30:.2f} GiB, recompute area "
+        f"{stage.recompute_bytes / 2**30:.2f} GiB")
+    s0, s1 = torch.cuda.Stream(), torch.cuda.Stream()
+    s0.wait_stream(torch.cuda.current_stream())
+    torch.cuda.synchronize()
+
+    def step():
+        stage.fwd(params, x, y, fwd_part, streams=(s0, s1))
+        stage.recompute(params, streams=(s0, s1))
+        stage.bwd(params, dy, dx, grads, False, bwd_part, streams=(s0, s1))
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"[bench] warmup done ({args.warmup} steps)")
+
+    stage.set_timing(B.KC_GEMM_DW)
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    start.record(s0)
+    for _ in range(args.steps):
+        step()
+    stop.record(s0)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    gpu_ms = start.elapsed_time(stop)
+    dw_ms, dw_launches = stage.read_timing()
+    stage.set_timing(B.KC_NONE)
+    ms_per_step = gpu_ms / args.steps
+    log(f"[bench] {args.steps} steps: {gpu_ms:.2f} ms on the GPU clock, {wall * 1e3:.2f} ms wall")
+
+    exe = flops.executed_flops(shape)
+    mdl = flops.model_flops(shape)
+    value = exe / (ms_per_step * 1e-3) / 1e12
+    dw_per_launch = flops.dw_gemm_flops(shape)
+    dw_avg_ms = dw_ms / max(dw_launches, 1)
+    achieved = dw_per_launch / (dw_avg_ms * 1e-3) / 1e12
+    traffic = dw_traffic_bytes()
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if shape.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": describe(shape), "global_batch": shape.micro_batch, "seq_len": shape.seq_len,
+                   "parallelism": f"tp{shape.tp_degree} shard on 1 GPU (cross-GPU reductions as hand-off buffers)"},
+        "pct_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
+        "executed_tflop_per_step": round(exe / 1e12, 4),
+        "model_tflop_per_step": round(mdl / 1e12, 4),
+        "model_tflops": round(mdl / (ms_per_step * 1e-3) / 1e12, 2),
+        "roofline": {
+            "kernel": "grouped weight-gradient GEMM (gemm_mfma_kernel, a_t=b_t=1, fp32 out), one launch per block",
+            "bound": "mfma",
+            "achieved": round(achieved, 2),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+            "traffic": traffic,
+            "launches_timed": dw_launches,
+            "avg_launch_ms": round(dw_avg_ms, 4),
+            "flop_per_launch": dw_per_launch,
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the oracle on the host (bounded sample)")
+        out["cpu_baseline"] = cpu_baseline(shape)
+    stage.close()
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

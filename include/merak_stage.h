@@ -179,6 +179,31 @@ int merak_stage_bwd(merak_stage_t stage, const void* params, const void* dy, voi
                     float* grads, int accumulate, void* bwd_partials, void* stream0,
                     void* stream1);
 
+/* Kernel classes the stage launches (for merak_stage_set_timing). */
+typedef enum {
+  MERAK_KC_NONE = 0,
+  MERAK_KC_GEMM_FWD = 1,   /* QKV, projection, FC1, FC2 GEMMs (forward and recompute)    */
+  MERAK_KC_GEMM_DX = 2,    /* input-gradient GEMMs of the backward pass                  */
+  MERAK_KC_GEMM_DW = 3,    /* grouped weight-gradient GEMM, one launch per block         */
+  MERAK_KC_ATTN_FWD = 4,   /* attention forward                                          */
+  MERAK_KC_ATTN_BWD = 5,   /* attention backward (delta, dK/dV and dQ kernels)           */
+  MERAK_KC_LN_FWD = 6,     /* LayerNorm forward                                          */
+  MERAK_KC_LN_BWD = 7,     /* LayerNorm backward (input gradient)                        */
+  MERAK_KC_REDUCE = 8,     /* bias / LayerNorm parameter gradient reductions             */
+  MERAK_KC_COUNT = 9
+} merak_kernel_class;
+
+/* Measurement aid: from now on, bracket every launch of `kernel_class` made by
+ * this handle with a pair of HIP events recorded on the stream the launch goes
+ * to (MERAK_KC_NONE turns it off).  At most 4096 launches are recorded between
+ * two reads.  Host-side bookkeeping only; results do not change. */
+int merak_stage_set_timing(merak_stage_t stage, int kernel_class);
+
+/* After the caller has synchronised: total milliseconds of the recorded launches
+ * (sum of per-launch event intervals) and their count; then clears the record.
+ * MERAK_ERR_ORDER if more than 4096 launches were made since the last read. */
+int merak_stage_read_timing(merak_stage_t stage, double* total_ms, int64_t* launches);
+
 /* ------------------------------------------------------------------------
  * Per-kernel entry points (each launches one hot-path kernel on `stream`).
  * They exist so each kernel can be checked and timed on its own; the stage

@@ -95,30 +95,38 @@ def causal_attention_forward(q, k, v):
     j > i, P = row softmax of S, O = P v.  Returns (O [b, s, heads, d], P [b, heads, s, s])."""
     d = q.shape[-1]
     s = q.shape[1]
-    S = np.einsum("bihd,bjhd->bhij", q, k) / math.sqrt(d)
+    qh, kh, vh = (t.transpose(0, 2, 1, 3) for t in (q, k, v))  # [b, heads, s, d]
+    S = (qh @ kh.transpose(0, 1, 3, 2)) / math.sqrt(d)
     future = np.triu(np.ones((s, s), dtype=bool), k=1)
     S = np.where(future, -np.inf, S)
     S = S - S.max(axis=-1, keepdims=True)
     E = np.exp(S)
     P = E / E.sum(axis=-1, keepdims=True)
-    O = np.einsum("bhij,bjhd->bihd", P, v)
+    O = (P @ vh).transpose(0, 2, 1, 3)
     return O, P
 
 
 def causal_attention_backward(dO, q, k, v, P):
     """Reverse mode of ``causal_attention_forward`` (softmax Jacobian written out)."""
     d = q.shape[-1]
-    dV = np.einsum("bhij,bihd->bjhd", P, dO)
-    dP = np.einsum("bihd,bjhd->bhij", dO, v)
+    qh, kh, vh, dOh = (t.transpose(0, 2, 1, 3) for t in (q, k, v, dO))  # [b, heads, s, d]
+    Pt = P.transpose(0, 1, 3, 2)
+    dV = Pt @ dOh
+    dP = dOh @ vh.transpose(0, 1, 3, 2)
     dS = P * (dP - (dP * P).sum(axis=-1, keepdims=True))
-    dQ = np.einsum("bhij,bjhd->bihd", dS, k) / math.sqrt(d)
-    dK = np.einsum("bhij,bihd->bjhd", dS, q) / math.sqrt(d)
-    return dQ, dK, dV
+    dQ = (dS @ kh) / math.sqrt(d)
+    dK = (dS.transpose(0, 1, 3, 2) @ qh) / math.sqrt(d)
+    return tuple(t.transpose(0, 2, 1, 3) for t in (dQ, dK, dV))
 
 
 # --------------------------------------------------------------------------
 # One block, t ranks (a list of shards); R = sum over the list
 # --------------------------------------------------------------------------
+
+def _tok_outer(a, b):
+    """sum over all tokens of a[t, i] * b[t, j] (a weight gradient dY^T X)."""
+    return a.reshape(-1, a.shape[-1]).T @ b.reshape(-1, b.shape[-1])
+
 
 def _split_heads(qkv, n_heads_local):
     b, s, three_hl = qkv.shape
@@ -176,8 +184,8 @@ def block_backward(dy, cache, shards: Sequence[Dict[str, np.ndarray]]):
     for r, (p, c) in enumerate(zip(shards, cache["ranks"])):
         dg = dy @ p["w2"]
         du = dg * gelu_grad(c["u"])
-        grads[r]["w2"] = np.einsum("bsi,bsj->ij", dy, c["g"])
-        grads[r]["w1"] = np.einsum("bsi,bsj->ij", du, cache["ln2"])
+        grads[r]["w2"] = _tok_outer(dy, c["g"])
+        grads[r]["w1"] = _tok_outer(du, cache["ln2"])
         grads[r]["b1"] = du.sum(axis=tok)
         d_ln2.append(du @ p["w1"])
         c["du"] = du
@@ -191,8 +199,8 @@ def block_backward(dy, cache, shards: Sequence[Dict[str, np.ndarray]]):
         dq, dk, dv = causal_attention_backward(dO, c["q"], c["k"], c["v"], c["P"])
         b, s = dx1.shape[:2]
         dqkv = np.concatenate([dq.reshape(b, s, -1), dk.reshape(b, s, -1), dv.reshape(b, s, -1)], axis=-1)
-        grads[r]["w_o"] = np.einsum("bsi,bsj->ij", dx1, c["O"])
-        grads[r]["w_qkv"] = np.einsum("bsi,bsj->ij", dqkv, cache["ln1"])
+        grads[r]["w_o"] = _tok_outer(dx1, c["O"])
+        grads[r]["w_qkv"] = _tok_outer(dqkv, cache["ln1"])
         grads[r]["b_qkv"] = dqkv.sum(axis=tok)
         d_ln1.append(dqkv @ p["w_qkv"])
         c["dqkv"] = dqkv

@@ -23,6 +23,8 @@ STATUS = {0: "MERAK_OK", -1: "MERAK_ERR_INVALID_ARG", -2: "MERAK_ERR_SHAPE", -3:
           -4: "MERAK_ERR_ALIGN", -5: "MERAK_ERR_WORKSPACE", -6: "MERAK_ERR_HIP", -7: "MERAK_ERR_UNSUPPORTED"}
 
 EPI_STORE, EPI_BIAS, EPI_BIAS_GELU, EPI_BIAS_RESID, EPI_GELU_BWD, EPI_F32 = range(6)
+(KC_NONE, KC_GEMM_FWD, KC_GEMM_DX, KC_GEMM_DW, KC_ATTN_FWD, KC_ATTN_BWD, KC_LN_FWD, KC_LN_BWD,
+ KC_REDUCE) = range(9)
 
 
 class MerakError(RuntimeError):
@@ -50,6 +52,8 @@ _SIGS = {
     "merak_stage_fwd": ([_P, _P, _P, _P, _P, _P, _P], _I),
     "merak_stage_recompute": ([_P, _P, _P, _P], _I),
     "merak_stage_bwd": ([_P, _P, _P, _P, _P, _I, _P, _P, _P], _I),
+    "merak_stage_set_timing": ([_P, _I], _I),
+    "merak_stage_read_timing": ([_P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)], _I),
     "merak_gemm": ([_I, _I, _I, _I, _I, _I, _I, _P, _I, _P, _I, _P, _P, _P, _P, _I, _P], _I),
     "merak_layernorm_fwd": ([_I, _I, _I, _F, _P, _P, _P, _P, _P, _P, _P], _I),
     "merak_reduce_scratch_elems": ([_I, _I], _SZ),
@@ -191,6 +195,16 @@ class Stage:
         _check(lib().merak_stage_bwd(self.handle, _ptr(params), _ptr(dy), _ptr(dx), _ptr(grads), int(accumulate),
                                      _ptr(bwd_partials), _stream(streams[0]), _stream(streams[1])),
                "merak_stage_bwd")
+
+    def set_timing(self, kernel_class: int) -> None:
+        _check(lib().merak_stage_set_timing(self.handle, kernel_class), "merak_stage_set_timing")
+
+    def read_timing(self):
+        """(total ms, launches) of the timed kernel class since the last read."""
+        ms, n = ctypes.c_double(), ctypes.c_int64()
+        _check(lib().merak_stage_read_timing(self.handle, ctypes.byref(ms), ctypes.byref(n)),
+               "merak_stage_read_timing")
+        return float(ms.value), int(n.value)
 
     def close(self) -> None:
         if getattr(self, "handle", None):

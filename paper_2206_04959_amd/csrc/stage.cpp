@@ -22,6 +22,7 @@
 #include <map>
 #include <mutex>
 #include <new>
+#include <vector>
 
 #include "../../include/merak_stage.h"
 #include "kernels.h"
@@ -31,6 +32,7 @@ using namespace merak;
 namespace {
 
 constexpr int kMaxBlocks = 64;
+constexpr int kMaxTimed = 4096;
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
@@ -212,6 +214,11 @@ struct merak_stage {
   hipEvent_t ev_fork, ev_s1, ev_j0, ev_j1, ev_aux, ev_dw[2];
   int state;  // 0 idle, 1 forward pending, 2 recomputed
   const void* x0;
+  // optional per-launch event timing of one kernel class
+  int timed_class;
+  std::vector<hipEvent_t> t_ev;  // 2 * kMaxTimed events, created on first use
+  int t_count;
+  bool t_overflow;
 };
 
 namespace {
@@ -241,6 +248,29 @@ char* block_acts(merak_stage* S, int l, int phase) {
     if (e_ != hipSuccess) return MERAK_ERR_HIP; \
   } while (0)
 
+// Run `launch` (returns hipError_t); if its kernel class is being timed, record
+// a start/stop event pair around it on `st`.
+template <typename F>
+int timed(merak_stage* S, int cls, hipStream_t st, F&& launch) {
+  const bool on = (S->timed_class == cls && cls != MERAK_KC_NONE);
+  if (on && S->t_count >= kMaxTimed) S->t_overflow = true;
+  const bool rec = on && S->t_count < kMaxTimed;
+  if (rec) HIP_TRY(hipEventRecord(S->t_ev[2 * S->t_count], st));
+  HIP_TRY(launch());
+  if (rec) {
+    HIP_TRY(hipEventRecord(S->t_ev[2 * S->t_count + 1], st));
+    ++S->t_count;
+  }
+  return MERAK_OK;
+}
+
+#define LAUNCH(cls, st, expr) TRY_INNER(timed(S, (cls), (st), [&]() { return (expr); }))
+#define TRY_INNER(expr)            \
+  do {                             \
+    int r2_ = (expr);              \
+    if (r2_ != MERAK_OK) return r2_; \
+  } while (0)
+
 inline const char* P(const void* params, const merak_stage* S, int l, int which) {
   return (const char*)params + (S->p_stride * l + S->p_off[which]) * S->D.esz;
 }
@@ -263,31 +293,31 @@ int block_forward(merak_stage* S, const void* params, int l, int j, char* A, con
   const size_t e = D.esz;
   const int M = D.Ms;
   // LN1
-  HIP_TRY(launch_layernorm_fwd(dt, M, D.h, D.eps, x + r0 * D.h * e, P(params, S, l, P_LN1G), P(params, S, l, P_LN1B),
+  LAUNCH(MERAK_KC_LN_FWD, st, launch_layernorm_fwd(dt, M, D.h, D.eps, x + r0 * D.h * e, P(params, S, l, P_LN1G), P(params, S, l, P_LN1B),
                                A + L.ln1 + r0 * D.h * e, (float*)(A + L.mu1) + r0, (float*)(A + L.rs1) + r0, st));
   // QKV (column parallel) + bias
   GemmProblem p = gp(M, 3 * D.hl, D.h, A + L.ln1 + r0 * D.h * e, D.h, P(params, S, l, P_WQKV), D.h,
                      A + L.qkv + r0 * 3 * D.hl * e, 3 * D.hl, P(params, S, l, P_BQKV));
-  HIP_TRY(launch_gemm(dt, false, false, EPI_BIAS, &p, 1, st));
+  LAUNCH(MERAK_KC_GEMM_FWD, st, launch_gemm(dt, false, false, EPI_BIAS, &p, 1, st));
   // causal attention on the local heads
-  HIP_TRY(launch_attention_fwd(dt, D.bs, D.s, D.al, D.d, A + L.qkv + r0 * 3 * D.hl * e, A + L.o + r0 * D.hl * e,
+  LAUNCH(MERAK_KC_ATTN_FWD, st, launch_attention_fwd(dt, D.bs, D.s, D.al, D.d, A + L.qkv + r0 * 3 * D.hl * e, A + L.o + r0 * D.hl * e,
                                (float*)(A + L.lse) + (size_t)j * D.bs * D.al * D.s, st));
   // projection (row parallel): partial sum -> hand-off; x1 = x + partial + b_o
   p = gp(M, D.h, D.hl, A + L.o + r0 * D.hl * e, D.hl, P(params, S, l, P_WO), D.hl, A + L.x1 + r0 * D.h * e, D.h,
          P(params, S, l, P_BO), x + r0 * D.h * e, part_o ? part_o + r0 * D.h * e : nullptr);
-  HIP_TRY(launch_gemm(dt, false, false, EPI_BIAS_RESID, &p, 1, st));
+  LAUNCH(MERAK_KC_GEMM_FWD, st, launch_gemm(dt, false, false, EPI_BIAS_RESID, &p, 1, st));
   // LN2
-  HIP_TRY(launch_layernorm_fwd(dt, M, D.h, D.eps, A + L.x1 + r0 * D.h * e, P(params, S, l, P_LN2G),
+  LAUNCH(MERAK_KC_LN_FWD, st, launch_layernorm_fwd(dt, M, D.h, D.eps, A + L.x1 + r0 * D.h * e, P(params, S, l, P_LN2G),
                                P(params, S, l, P_LN2B), A + L.ln2 + r0 * D.h * e, (float*)(A + L.mu2) + r0,
                                (float*)(A + L.rs2) + r0, st));
   // FC1 (column parallel) + bias + GeLU; keeps the pre-activation u
   p = gp(M, D.fl, D.h, A + L.ln2 + r0 * D.h * e, D.h, P(params, S, l, P_W1), D.h, A + L.g + r0 * D.fl * e, D.fl,
          P(params, S, l, P_B1), nullptr, A + L.u + r0 * D.fl * e);
-  HIP_TRY(launch_gemm(dt, false, false, EPI_BIAS_GELU, &p, 1, st));
+  LAUNCH(MERAK_KC_GEMM_FWD, st, launch_gemm(dt, false, false, EPI_BIAS_GELU, &p, 1, st));
   // FC2 (row parallel): partial sum -> hand-off; y = x1 + partial + b2
   p = gp(M, D.h, D.fl, A + L.g + r0 * D.fl * e, D.fl, P(params, S, l, P_W2), D.fl, y + r0 * D.h * e, D.h,
          P(params, S, l, P_B2), A + L.x1 + r0 * D.h * e, part_f ? part_f + r0 * D.h * e : nullptr);
-  HIP_TRY(launch_gemm(dt, false, false, EPI_BIAS_RESID, &p, 1, st));
+  LAUNCH(MERAK_KC_GEMM_FWD, st, launch_gemm(dt, false, false, EPI_BIAS_RESID, &p, 1, st));
   return MERAK_OK;
 }
 
@@ -304,28 +334,28 @@ int block_backward_chain(merak_stage* S, const void* params, int l, int j, const
   // FC2 backward: dg = dy W2; du = dg * gelu'(u)
   GemmProblem p = gp(M, D.fl, D.h, dy + r0 * D.h * e, D.h, P(params, S, l, P_W2), D.fl, B + Bl.du + r0 * D.fl * e,
                      D.fl, nullptr, nullptr, (void*)(A + L.u + r0 * D.fl * e));
-  HIP_TRY(launch_gemm(dt, false, true, EPI_GELU_BWD, &p, 1, st));
+  LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(dt, false, true, EPI_GELU_BWD, &p, 1, st));
   // FC1 backward: d_ln2 partial = du W1 (hand-off)
   p = gp(M, D.h, D.fl, B + Bl.du + r0 * D.fl * e, D.fl, P(params, S, l, P_W1), D.h, d_ln2 + r0 * D.h * e, D.h);
-  HIP_TRY(launch_gemm(dt, false, true, EPI_STORE, &p, 1, st));
+  LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(dt, false, true, EPI_STORE, &p, 1, st));
   // LN2 backward + residual gradient: dx1 = dy + LN2'(d_ln2)
-  HIP_TRY(launch_layernorm_bwd(dt, M, D.h, d_ln2 + r0 * D.h * e, A + L.x1 + r0 * D.h * e,
+  LAUNCH(MERAK_KC_LN_BWD, st, launch_layernorm_bwd(dt, M, D.h, d_ln2 + r0 * D.h * e, A + L.x1 + r0 * D.h * e,
                                (const float*)(A + L.mu2) + r0, (const float*)(A + L.rs2) + r0,
                                P(params, S, l, P_LN2G), dy + r0 * D.h * e, B + Bl.dx1 + r0 * D.h * e, st));
   // projection backward: dO = dx1 W_o
   p = gp(M, D.hl, D.h, B + Bl.dx1 + r0 * D.h * e, D.h, P(params, S, l, P_WO), D.hl, B + Bl.dO + r0 * D.hl * e, D.hl);
-  HIP_TRY(launch_gemm(dt, false, true, EPI_STORE, &p, 1, st));
+  LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(dt, false, true, EPI_STORE, &p, 1, st));
   // attention backward -> dqkv
   const size_t lse_off = (size_t)j * D.bs * D.al * D.s;
-  HIP_TRY(launch_attention_bwd(dt, D.bs, D.s, D.al, D.d, A + L.qkv + r0 * 3 * D.hl * e, A + L.o + r0 * D.hl * e,
+  LAUNCH(MERAK_KC_ATTN_BWD, st, launch_attention_bwd(dt, D.bs, D.s, D.al, D.d, A + L.qkv + r0 * 3 * D.hl * e, A + L.o + r0 * D.hl * e,
                                (const float*)(A + L.lse) + lse_off, B + Bl.dO + r0 * D.hl * e,
                                B + Bl.dqkv + r0 * 3 * D.hl * e, (float*)(B + Bl.delta) + lse_off, st));
   // QKV backward: d_ln1 partial = dqkv W_qkv (hand-off)
   p = gp(M, D.h, 3 * D.hl, B + Bl.dqkv + r0 * 3 * D.hl * e, 3 * D.hl, P(params, S, l, P_WQKV), D.h,
          d_ln1 + r0 * D.h * e, D.h);
-  HIP_TRY(launch_gemm(dt, false, true, EPI_STORE, &p, 1, st));
+  LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(dt, false, true, EPI_STORE, &p, 1, st));
   // LN1 backward + residual gradient: dx = dx1 + LN1'(d_ln1)
-  HIP_TRY(launch_layernorm_bwd(dt, M, D.h, d_ln1 + r0 * D.h * e, x + r0 * D.h * e, (const float*)(A + L.mu1) + r0,
+  LAUNCH(MERAK_KC_LN_BWD, st, launch_layernorm_bwd(dt, M, D.h, d_ln1 + r0 * D.h * e, x + r0 * D.h * e, (const float*)(A + L.mu1) + r0,
                                (const float*)(A + L.rs1) + r0, P(params, S, l, P_LN1G), B + Bl.dx1 + r0 * D.h * e,
                                dx + r0 * D.h * e, st));
   return MERAK_OK;
@@ -347,35 +377,35 @@ int block_param_grads(merak_stage* S, int l, const char* A, const char* x, const
   p[1] = gp(D.h, D.hl, T, B + Bl.dx1, D.h, A + L.o, D.hl, g + S->p_off[P_WO], D.hl, nullptr, nullptr, nullptr, acc);
   p[2] = gp(D.fl, D.h, T, B + Bl.du, D.fl, A + L.ln2, D.h, g + S->p_off[P_W1], D.h, nullptr, nullptr, nullptr, acc);
   p[3] = gp(D.h, D.fl, T, dy, D.h, A + L.g, D.fl, g + S->p_off[P_W2], D.fl, nullptr, nullptr, nullptr, acc);
-  HIP_TRY(launch_gemm(dt, true, true, EPI_F32, p, 4, st));
+  LAUNCH(MERAK_KC_GEMM_DW, st, launch_gemm(dt, true, true, EPI_F32, p, 4, st));
   // bias gradients: token sums of the layer output gradients
   const int G = (int)reduce_groups(T);
   float* pb;
   pb = (float*)(B + Bl.p_bqkv);
-  HIP_TRY(launch_column_partials(dt, T, 3 * D.hl, B + Bl.dqkv, pb, st));
-  HIP_TRY(launch_reduce_partials(G, 3 * D.hl, pb, g + S->p_off[P_BQKV], acc, st));
+  LAUNCH(MERAK_KC_REDUCE, st, launch_column_partials(dt, T, 3 * D.hl, B + Bl.dqkv, pb, st));
+  LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials(G, 3 * D.hl, pb, g + S->p_off[P_BQKV], acc, st));
   pb = (float*)(B + Bl.p_bo);
-  HIP_TRY(launch_column_partials(dt, T, D.h, B + Bl.dx1, pb, st));
-  HIP_TRY(launch_reduce_partials(G, D.h, pb, g + S->p_off[P_BO], acc, st));
+  LAUNCH(MERAK_KC_REDUCE, st, launch_column_partials(dt, T, D.h, B + Bl.dx1, pb, st));
+  LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials(G, D.h, pb, g + S->p_off[P_BO], acc, st));
   pb = (float*)(B + Bl.p_b1);
-  HIP_TRY(launch_column_partials(dt, T, D.fl, B + Bl.du, pb, st));
-  HIP_TRY(launch_reduce_partials(G, D.fl, pb, g + S->p_off[P_B1], acc, st));
+  LAUNCH(MERAK_KC_REDUCE, st, launch_column_partials(dt, T, D.fl, B + Bl.du, pb, st));
+  LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials(G, D.fl, pb, g + S->p_off[P_B1], acc, st));
   pb = (float*)(B + Bl.p_b2);
-  HIP_TRY(launch_column_partials(dt, T, D.h, dy, pb, st));
-  HIP_TRY(launch_reduce_partials(G, D.h, pb, g + S->p_off[P_B2], acc, st));
+  LAUNCH(MERAK_KC_REDUCE, st, launch_column_partials(dt, T, D.h, dy, pb, st));
+  LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials(G, D.h, pb, g + S->p_off[P_B2], acc, st));
   // LayerNorm parameters
   float* pg = (float*)(B + Bl.p_g2);
   float* pbe = (float*)(B + Bl.p_be2);
-  HIP_TRY(launch_layernorm_param_partials(dt, T, D.h, d_ln2, A + L.x1, (const float*)(A + L.mu2),
+  LAUNCH(MERAK_KC_REDUCE, st, launch_layernorm_param_partials(dt, T, D.h, d_ln2, A + L.x1, (const float*)(A + L.mu2),
                                           (const float*)(A + L.rs2), pg, pbe, st));
-  HIP_TRY(launch_reduce_partials(G, D.h, pg, g + S->p_off[P_LN2G], acc, st));
-  HIP_TRY(launch_reduce_partials(G, D.h, pbe, g + S->p_off[P_LN2B], acc, st));
+  LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials(G, D.h, pg, g + S->p_off[P_LN2G], acc, st));
+  LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials(G, D.h, pbe, g + S->p_off[P_LN2B], acc, st));
   pg = (float*)(B + Bl.p_g1);
   pbe = (float*)(B + Bl.p_be1);
-  HIP_TRY(launch_layernorm_param_partials(dt, T, D.h, d_ln1, x, (const float*)(A + L.mu1), (const float*)(A + L.rs1),
+  LAUNCH(MERAK_KC_REDUCE, st, launch_layernorm_param_partials(dt, T, D.h, d_ln1, x, (const float*)(A + L.mu1), (const float*)(A + L.rs1),
                                           pg, pbe, st));
-  HIP_TRY(launch_reduce_partials(G, D.h, pg, g + S->p_off[P_LN1G], acc, st));
-  HIP_TRY(launch_reduce_partials(G, D.h, pbe, g + S->p_off[P_LN1B], acc, st));
+  LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials(G, D.h, pg, g + S->p_off[P_LN1G], acc, st));
+  LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials(G, D.h, pbe, g + S->p_off[P_LN1B], acc, st));
   return MERAK_OK;
 }
 
@@ -472,6 +502,9 @@ int merak_stage_create(const merak_stage_config* cfg, void* workspace, size_t wo
   S->rc = (char*)recompute_area;
   S->state = ST_IDLE;
   S->x0 = nullptr;
+  S->timed_class = MERAK_KC_NONE;
+  S->t_count = 0;
+  S->t_overflow = false;
   hipError_t e = hipStreamCreateWithFlags(&S->aux, hipStreamNonBlocking);
   const bool have_stream = (e == hipSuccess);
   hipEvent_t* evs[] = {&S->ev_fork, &S->ev_s1, &S->ev_j0, &S->ev_j1, &S->ev_aux, &S->ev_dw[0], &S->ev_dw[1]};
@@ -500,8 +533,43 @@ int merak_stage_destroy(merak_stage_t S) {
   }
   hipEvent_t evs[] = {S->ev_fork, S->ev_s1, S->ev_j0, S->ev_j1, S->ev_aux, S->ev_dw[0], S->ev_dw[1]};
   for (hipEvent_t ev : evs) (void)hipEventDestroy(ev);
+  for (hipEvent_t ev : S->t_ev) (void)hipEventDestroy(ev);
   (void)hipStreamDestroy(S->aux);
   delete S;
+  return MERAK_OK;
+}
+
+int merak_stage_set_timing(merak_stage_t S, int kernel_class) {
+  if (!S) return MERAK_ERR_INVALID_ARG;
+  if (kernel_class < MERAK_KC_NONE || kernel_class >= MERAK_KC_COUNT) return MERAK_ERR_INVALID_ARG;
+  if (kernel_class != MERAK_KC_NONE && S->t_ev.empty()) {
+    S->t_ev.resize(2 * kMaxTimed);
+    for (size_t i = 0; i < S->t_ev.size(); ++i) {
+      if (hipEventCreate(&S->t_ev[i]) != hipSuccess) {
+        for (size_t k = 0; k < i; ++k) (void)hipEventDestroy(S->t_ev[k]);
+        S->t_ev.clear();
+        return MERAK_ERR_HIP;
+      }
+    }
+  }
+  S->timed_class = kernel_class;
+  S->t_count = 0;
+  S->t_overflow = false;
+  return MERAK_OK;
+}
+
+int merak_stage_read_timing(merak_stage_t S, double* total_ms, int64_t* launches) {
+  if (!S || !total_ms || !launches) return MERAK_ERR_INVALID_ARG;
+  if (S->t_overflow) return MERAK_ERR_ORDER;
+  double sum = 0.0;
+  for (int i = 0; i < S->t_count; ++i) {
+    float ms = 0.0f;
+    HIP_TRY(hipEventElapsedTime(&ms, S->t_ev[2 * i], S->t_ev[2 * i + 1]));
+    sum += ms;
+  }
+  *total_ms = sum;
+  *launches = S->t_count;
+  S->t_count = 0;
   return MERAK_OK;
 }
 

@@ -1,0 +1,40 @@
+"""Algorithmic work of one stage step (counted as the method must compute it).
+
+Per block forward, one rank's shard, T = b*s tokens:
+  GEMMs      2*T*h*(3h/t) + 2*T*(h/t)*h + 2*T*h*(f/t) + 2*T*(f/t)*h
+  attention  2*b*(h/t)*s*(s+1)   (causal: Q K^T and P V over the lower triangle
+                                  including the diagonal)
+The backward pass costs twice the forward (Sec. 5.1 of the paper takes the same
+ratio), and each recomputed block repeats its forward once.  Tile padding and
+the attention backward's rebuilding of P are not counted.
+"""
+from __future__ import annotations
+
+from .synth import StageShape
+
+
+def block_forward_flops(s: StageShape) -> float:
+    T, h, hl, fl = s.tokens, s.hidden, s.local_hidden, s.local_ffn
+    gemm = 2.0 * T * h * (3 * hl) + 2.0 * T * hl * h + 2.0 * T * h * fl + 2.0 * T * fl * h
+    attn = 2.0 * s.micro_batch * hl * s.seq_len * (s.seq_len + 1)
+    return gemm + attn
+
+
+def recomputed_blocks(s: StageShape) -> int:
+    return bin(s.recompute_mask).count("1")
+
+
+def executed_flops(s: StageShape) -> float:
+    """Forward + recompute + backward of the whole stage for one micro-batch."""
+    return (3 * s.n_blocks + recomputed_blocks(s)) * block_forward_flops(s)
+
+
+def model_flops(s: StageShape) -> float:
+    """Forward + backward only (what the stage would cost without recomputation)."""
+    return 3 * s.n_blocks * block_forward_flops(s)
+
+
+def dw_gemm_flops(s: StageShape) -> float:
+    """The grouped weight-gradient GEMM of one block (= the block's forward GEMM work)."""
+    T, h, hl, fl = s.tokens, s.hidden, s.local_hidden, s.local_ffn
+    return 2.0 * T * (3 * hl * h + h * hl + fl * h + h * fl)
