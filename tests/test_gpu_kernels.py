@@ -136,12 +136,13 @@ def test_column_sum(dtype):
     assert rel_err(out.cpu().numpy(), 2 * x.sum(0)) < 1e-5
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
-@pytest.mark.parametrize("d", [64, 96, 128])
-@pytest.mark.parametrize("seq", [128, 320])
-def test_attention_fwd_bwd(dtype, d, seq):
+ATTN_CASES = [(dt, d, s, 2, 3) for dt in ("bf16", "fp32") for d in (64, 96, 128) for s in (128, 320)]
+ATTN_CASES += [("bf16", 128, 2048, 1, 2), ("bf16", 96, 1024, 2, 2)]  # full-length rows of the workloads
+
+
+@pytest.mark.parametrize("dtype,d,seq,batch,heads", ATTN_CASES)
+def test_attention_fwd_bwd(dtype, d, seq, batch, heads):
     torch = need_gpu()
-    batch, heads = 2, 3
     print(f"[attention] {dtype} d={d} seq={seq}", flush=True)
     qkv_p, qkv = _rand((batch, seq, 3, heads, d), dtype, 14 + d + seq)
     do_p, do = _rand((batch, seq, heads, d), dtype, 15 + d + seq)
