@@ -233,6 +233,13 @@ int merak_gemm(int dtype, int a_trans, int b_trans, int epilogue, int M, int N, 
                const void* a, int lda, const void* b, int ldb, void* c, const void* bias,
                const void* resid, void* aux, int accumulate, void* stream);
 
+/* Tile-shape override of the bf16 GEMM kernel, for tests and tuning:
+ * 0 restores the built-in choice, 1..8 force one shape (256x256/4 waves/2
+ * stages, 256x128/4/3, 128x256/4/3, 128x128/4/2, 128x128/4/3, 128x128/4/4,
+ * 256x256/8/2, 256x128/8/3).  Process-wide; returns the previous value, or -1
+ * for an out-of-range cfg (nothing changed).  Host-only, not thread-safe. */
+int merak_gemm_tile_override(int cfg);
+
 /* LayerNorm forward over `rows` rows of width h (h % 8 == 0, h <= 8192):
  * y = gamma * (x - mean) * rstd + beta; mean and rstd fp32 [rows]. */
 int merak_layernorm_fwd(int dtype, int rows, int h, float eps, const void* x, const void* gamma,

@@ -55,6 +55,7 @@ _SIGS = {
     "merak_stage_set_timing": ([_P, _I], _I),
     "merak_stage_read_timing": ([_P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)], _I),
     "merak_gemm": ([_I, _I, _I, _I, _I, _I, _I, _P, _I, _P, _I, _P, _P, _P, _P, _I, _P], _I),
+    "merak_gemm_tile_override": ([_I], _I),
     "merak_layernorm_fwd": ([_I, _I, _I, _F, _P, _P, _P, _P, _P, _P, _P], _I),
     "merak_reduce_scratch_elems": ([_I, _I], _SZ),
     "merak_layernorm_bwd": ([_I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _P, _P], _I),
@@ -235,6 +236,15 @@ def gemm(a, b, c, M, N, K, a_trans=False, b_trans=False, epilogue=EPI_STORE, bia
     _check(lib().merak_gemm(dt, int(a_trans), int(b_trans), epilogue, M, N, K, _ptr(a), lda, _ptr(b), ldb,
                             _ptr(c), _ptr(bias), _ptr(resid), _ptr(aux), int(accumulate), _stream(stream)),
            "merak_gemm")
+
+
+def gemm_tile_override(cfg: int) -> int:
+    """Force a bf16 GEMM tile shape (1..8) or restore the built-in choice (0);
+    returns the previous setting."""
+    prev = int(lib().merak_gemm_tile_override(int(cfg)))
+    if prev < 0:
+        raise ValueError(f"tile configuration {cfg} out of range")
+    return prev
 
 
 def layernorm_fwd(x, gamma, beta, y, mean, rstd, eps=1e-5, stream=None) -> None:

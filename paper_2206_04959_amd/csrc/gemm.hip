@@ -4,19 +4,22 @@
 //   backward  dY W       (A row-major [M,K], B = weight [K,N])          a_t=0 b_t=1
 //   weights   dY^T X     (A = dY [K,M] read transposed, B = X [K,N])    a_t=1 b_t=1
 //
-// bf16 path: v_mfma_f32_32x32x16_bf16 on LDS-staged tiles (BK = 64), fp32
-// accumulation in registers, double-buffered LDS with one barrier per K step,
-// register prefetch of the next K tile while the current one is multiplied.
-// Both operands are kept K-contiguous in LDS (rows padded by 8 elements so the
-// 16-byte fragment reads of 8 consecutive rows hit distinct banks); an operand
-// that is contiguous along M or N in memory is loaded as 8x8 blocks and
-// transposed in registers on its way into LDS.  The MFMA is issued with the B
-// tile as its first operand so each lane ends up owning one output row and 4
-// consecutive output columns per group, which the fused epilogues store as one
-// vector.
+// bf16 path: v_mfma_f32_32x32x16_bf16 with fp32 accumulation.  Operand tiles
+// (BK = 64) go from global memory straight into an LDS ring (buffer loads that
+// write LDS, no register staging) in XOR-swizzled layouts chosen for the 64
+// banks of gfx950 LDS; operands contiguous along M or N stay that way in LDS
+// and are read with the transposing LDS read, so no operand is transposed in
+// registers.  Each wave reads the fragments of the next K sub-step while the
+// MFMAs of the current one run, with one workgroup barrier per K stage.  The
+// MFMA takes the B tile as its first operand so each lane owns one output row
+// and 4 consecutive columns per group, which the fused epilogues store as one
+// vector.  Workgroups are mapped to tiles so that each of the 8 XCDs works on
+// a compact block of neighbouring tiles (operand reuse in its own L2).
 //
 // fp32 check mode: a plain LDS-tiled FMA kernel with the same layouts and
 // epilogues.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -95,115 +98,175 @@ __device__ __forceinline__ GemmProblem select_problem(const GemmBatch& b, int bi
 
 // ---------------------------------------------------------------------------
 // bf16 MFMA kernel
+//
+// LDS stage (one BK = 64 slice of K) of an operand with R tile rows (R = BM
+// for A, BN for B) occupies R * 128 bytes, in one of two layouts:
+//   K-contiguous operand: [R][64 k]; the 16-byte chunk c of row r is stored in
+//     slot c ^ ((r >> 1) & 7), so the 16 rows read by one 256-byte pass of a
+//     fragment read land in distinct banks (gfx950 LDS: 64 banks of 4 bytes);
+//   MN-contiguous operand: [64 k][R]; chunk c of k-row k is stored in slot
+//     c ^ (4 * (k & 3)), so the four k-rows of a transposing read pass are
+//     spread over the 256-byte bank space.
+// Tiles move global -> LDS with buffer loads that write LDS directly (no VGPR
+// staging); each wave instruction fills 1 KiB of LDS, lane i writing bytes
+// [16 i, 16 i + 16), and the swizzle is applied by choosing which global
+// chunk each lane fetches.  Rows or columns past the operand's extent read as
+// zero (buffer range check) or as in-range data whose products land only in
+// discarded outputs.  MN-contiguous fragments are read with the gfx950
+// transposing LDS read (ds_read_b64_tr_b16), which hands lane i of each
+// 16-lane group the i-th column of the 4 x 16 block its group fetched.
 // ---------------------------------------------------------------------------
 constexpr int kBK = 64;
-constexpr int kLDK = kBK + 8;  // padded LDS row, elements
 
-// Global -> register -> LDS staging of one BK-wide K tile of an operand with R
-// rows (R = BM for A, BN for B).  Each thread owns kRegs 16-byte registers.
-//
-// K-contiguous operand (element (r, k) at base[r*ld + k]): 16-byte chunks,
-// 8 per row; consecutive threads read consecutive chunks of a row.
-//
-// R-contiguous operand (element (r, k) at base[k*ld + r]): 8x8 blocks (8 k rows
-// x 8 contiguous r), transposed in registers so LDS stays K-contiguous.
-template <bool TRANS, int R, int NT>
-struct Stage {
-  static constexpr int kChunks = R * kBK / 8;             // K-contiguous: 16-byte chunks
-  static constexpr int kBlocks = (R / 8) * (kBK / 8);     // R-contiguous: 8x8 blocks
-  static constexpr int kBlocksPer = (kBlocks + NT - 1) / NT;
-  static_assert(TRANS || kChunks % NT == 0, "tile/thread mismatch");
-  static constexpr int kRegs = TRANS ? kBlocksPer * 8 : kChunks / NT;
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+#define MERAK_LDS __attribute__((address_space(3)))
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t operand_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+
+// Workgroup id -> tile id such that each of the 8 XCDs (which receive
+// workgroups round-robin) works on one contiguous range of tiles.
+__device__ __forceinline__ int xcd_remap(int bid, int n) {
+  const int per = n >> 3, rem = n & 7, x = bid & 7, idx = bid >> 3;
+  return (x < rem ? x * (per + 1) : rem * (per + 1) + (x - rem) * per) + idx;
+}
+
+// Global -> LDS loader of one operand.  Each wave issues kInst 16-byte-per-lane
+// loads per K stage.
+template <bool TRANS, int R, int NW>
+struct TileLoader {
+  static constexpr int kInst = R / 8 / NW;
+  static_assert(R / 8 % NW == 0, "tile rows must split evenly over the waves");
+  static_assert(!TRANS || R == 128 || R == 256, "MN-contiguous tiles must be 128 or 256 wide");
+  uint32_t voff[kInst];
+  uint32_t step;  // bytes to advance per K stage
+
+  __device__ __forceinline__ void init(int r0, int ld, int wave, int lane) {
+#pragma unroll
+    for (int q = 0; q < kInst; ++q) {
+      if constexpr (!TRANS) {
+        const int row = (q * NW + wave) * 8 + (lane >> 3);
+        const int chunk = (lane & 7) ^ ((row >> 1) & 7);
+        voff[q] = (uint32_t)((r0 + row) * ld + chunk * 8) * 2u;
+      } else {
+        constexpr int CPR = R / 8;     // 16-byte chunks per k-row
+        constexpr int KPI = 64 / CPR;  // k-rows per wave instruction
+        const int kr = (q * NW + wave) * KPI + lane / CPR;
+        const int chunk = (lane % CPR) ^ ((kr & 3) << 2);
+        voff[q] = (uint32_t)(kr * ld + r0 + chunk * 8) * 2u;
+      }
+    }
+    step = TRANS ? (uint32_t)(kBK * ld * 2) : (uint32_t)(kBK * 2);
+  }
+
+  // Issue load q of the current K stage into `lds` (R * 128 bytes); after the
+  // last one (q = kInst - 1) the loader moves on to the next stage.
+  __device__ __forceinline__ void issue_one(__amdgpu_buffer_rsrc_t rsrc, char* lds, int wave, int q) {
+    const int slot = __builtin_amdgcn_readfirstlane((q * NW + wave) * 1024);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (MERAK_LDS void*)(lds + slot), 16, (int)voff[q], 0, 0, 0);
+    voff[q] += step;
+  }
+
+  // Issue the loads of the current K stage into `lds` (R * 128 bytes) and move
+  // on to the next stage.
+  __device__ __forceinline__ void issue(__amdgpu_buffer_rsrc_t rsrc, char* lds, int wave) {
+#pragma unroll
+    for (int q = 0; q < kInst; ++q) {
+      const int slot = __builtin_amdgcn_readfirstlane((q * NW + wave) * 1024);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (MERAK_LDS void*)(lds + slot), 16, (int)voff[q], 0, 0, 0);
+      voff[q] += step;
+    }
+  }
 };
 
-template <bool TRANS, int R, int NT, int NR>
-__device__ __forceinline__ void stage_load(u32x4_t (&r)[NR], const bf16_t* base, int ld, int r0, int rtot,
-                                           int k0, int tid) {
-  if constexpr (!TRANS) {
-#pragma unroll
-    for (int i = 0; i < NR; ++i) {
-      const int c = tid + i * NT;
-      const int row = min(r0 + (c >> 3), rtot - 1);
-      r[i] = *reinterpret_cast<const u32x4_t*>(base + (size_t)row * ld + k0 + (c & 7) * 8);
-    }
-  } else {
-    constexpr int kBlocks = Stage<TRANS, R, NT>::kBlocks;
-#pragma unroll
-    for (int i = 0; i < NR / 8; ++i) {
-      const int c = tid + i * NT;
-      if (kBlocks % NT == 0 || c < kBlocks) {
-        const int kg = c & 7;
-        const int rs = min(r0 + (c >> 3) * 8, rtot - 8);
-        const bf16_t* p = base + (size_t)(k0 + kg * 8) * ld + rs;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) r[i * 8 + j] = *reinterpret_cast<const u32x4_t*>(p + (size_t)j * ld);
-      }
+// Fragment reader: the 32 x 16 (rows x k) MFMA operand block starting at tile
+// row `row0` (a multiple of 32) and k = 16 * ks of an LDS stage.  Lane l gets
+// row row0 + l % 32 and k = 16 ks + 8 (l / 32) + 0..7.
+template <bool TRANS, int R>
+struct FragReader {
+  static constexpr int kInstPerFrag = TRANS ? 2 : 1;  // LDS read instructions per fragment
+  int lane_off;  // lane-dependent part of the byte offset
+  int key;       // lane-dependent swizzle term
+
+  __device__ __forceinline__ void init(int lane) {
+    if constexpr (!TRANS) {
+      lane_off = (lane & 31) * 128;
+      key = (lane >> 5) ^ (((lane & 31) >> 1) & 7);
+    } else {
+      const int b = lane >> 4, j = lane & 15;
+      lane_off = ((b >> 1) * 8 + (j >> 2)) * (2 * R) + ((b & 1) * 2 + ((j >> 1) & 1)) * 16 + (j & 1) * 8;
+      key = (j >> 2) << 2;
     }
   }
-}
 
-__device__ __forceinline__ uint32_t u4_word(const u32x4_t& v, int w) { return v[w]; }
-
-template <bool TRANS, int R, int NT, int NR>
-__device__ __forceinline__ void stage_store(const u32x4_t (&r)[NR], bf16_t* s, int tid) {
-  if constexpr (!TRANS) {
-#pragma unroll
-    for (int i = 0; i < NR; ++i) {
-      const int c = tid + i * NT;
-      *reinterpret_cast<u32x4_t*>(s + (c >> 3) * kLDK + (c & 7) * 8) = r[i];
-    }
-  } else {
-    constexpr int kBlocks = Stage<TRANS, R, NT>::kBlocks;
-#pragma unroll
-    for (int i = 0; i < NR / 8; ++i) {
-      const int c = tid + i * NT;
-      if (kBlocks % NT == 0 || c < kBlocks) {
-        const int kg = c & 7;
-        const int rb = (c >> 3) * 8;
-        // Output row rb+e holds k = kg*8 + 0..7, i.e. element e of r[i*8 + 0..7].
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          uint32_t o[4];
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const uint32_t lo = u4_word(r[i * 8 + 2 * q], e >> 1);
-            const uint32_t hi = u4_word(r[i * 8 + 2 * q + 1], e >> 1);
-            o[q] = (e & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
-          }
-          *reinterpret_cast<u32x4_t*>(s + (rb + e) * kLDK + kg * 8) = u32x4_t{o[0], o[1], o[2], o[3]};
-        }
-      }
+  __device__ __forceinline__ bf16x8_t read(const char* lds, int row0, int ks) const {
+    if constexpr (!TRANS) {
+      const char* p = lds + row0 * 128 + lane_off + (((2 * ks) ^ key) << 4);
+      return *reinterpret_cast<const bf16x8_t*>(p);
+    } else {
+      const char* p = lds + ks * 16 * (2 * R) + ((((row0 >> 3)) ^ key) << 4) + lane_off;
+      s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((MERAK_LDS s16x4_t*)(p));
+      s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((MERAK_LDS s16x4_t*)(p + 4 * (2 * R)));
+      s16x4_t v01 = lo, v23 = hi;
+      typedef short s16x8_t __attribute__((ext_vector_type(8)));
+      s16x8_t v = {v01[0], v01[1], v01[2], v01[3], v23[0], v23[1], v23[2], v23[3]};
+      return __builtin_bit_cast(bf16x8_t, v);
     }
   }
+};
+
+// Wait until at most N of this wave's vector-memory loads are outstanding and
+// all its LDS reads have completed, then join the workgroup barrier.  (The
+// buffer loads that write LDS directly are tracked by vmcnt only.)
+template <int N>
+__device__ __forceinline__ void wait_vm_barrier() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
 }
 
-template <int BM, int BN, int WM, int WN, bool A_T, bool B_T, int EPI>
+template <int BM, int BN, int WM, int WN, int NS, bool A_T, bool B_T, int EPI>
 __global__ void __launch_bounds__(WM * WN * 64) gemm_mfma_kernel(GemmBatch batch) {
-  constexpr int NT = WM * WN * 64;
-  constexpr int TM = BM / WM / 32;
-  constexpr int TN = BN / WN / 32;
-  extern __shared__ __align__(16) bf16_t smem[];
-  bf16_t* As = smem;                      // [2][BM][kLDK]
-  bf16_t* Bs = smem + 2 * BM * kLDK;      // [2][BN][kLDK]
+  constexpr int NW = WM * WN;
+  constexpr int WTM = BM / WM, WTN = BN / WN;  // wave tile
+  constexpr int TM = WTM / 32, TN = WTN / 32;
+  constexpr int A_BYTES = BM * 128, STAGE = (BM + BN) * 128;
+  extern __shared__ __align__(16) char smem[];
 
-  const int bid = blockIdx.x;
+  const int tile_id = xcd_remap(blockIdx.x, batch.tile_start[kMaxGroup]);
   int tile0;
-  const GemmProblem p = select_problem(batch, bid, &tile0);
-  const int tile = bid - tile0;
-  const int tiles_n = (p.N + BN - 1) / BN;
-  const int m0 = (tile / tiles_n) * BM;
-  const int n0 = (tile % tiles_n) * BN;
+  const GemmProblem p = select_problem(batch, tile_id, &tile0);
+  const int tile = tile_id - tile0;
+  const int tiles_m = (p.M + BM - 1) / BM, tiles_n = (p.N + BN - 1) / BN;
+  // Groups of 4 tile rows walked column by column, so that neighbouring tiles
+  // (same XCD) share operand panels in L2.
+  constexpr int GM = 4;
+  const int group = tile / (GM * tiles_n);
+  const int first_m = group * GM;
+  const int gsz = min(tiles_m - first_m, GM);
+  const int in_group = tile - group * GM * tiles_n;
+  const int m0 = (first_m + in_group % gsz) * BM;
+  const int n0 = (in_group / gsz) * BN;
 
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wave / WN, wn = wave % WN;
 
-  const bf16_t* A = reinterpret_cast<const bf16_t*>(p.a);
-  const bf16_t* B = reinterpret_cast<const bf16_t*>(p.b);
+  const uint32_t a_bytes = A_T ? (uint32_t)(((size_t)(p.K - 1) * p.lda + p.M) * 2)
+                               : (uint32_t)(((size_t)(p.M - 1) * p.lda + p.K) * 2);
+  const uint32_t b_bytes = B_T ? (uint32_t)(((size_t)(p.K - 1) * p.ldb + p.N) * 2)
+                               : (uint32_t)(((size_t)(p.N - 1) * p.ldb + p.K) * 2);
+  const __amdgpu_buffer_rsrc_t ra = operand_rsrc(p.a, a_bytes);
+  const __amdgpu_buffer_rsrc_t rb = operand_rsrc(p.b, b_bytes);
 
-  u32x4_t ra[Stage<A_T, BM, NT>::kRegs];
-  u32x4_t rb[Stage<B_T, BN, NT>::kRegs];
+  TileLoader<A_T, BM, NW> la;
+  TileLoader<B_T, BN, NW> lb;
+  la.init(m0, p.lda, wave, lane);
+  lb.init(n0, p.ldb, wave, lane);
+  FragReader<A_T, BM> fa;
+  FragReader<B_T, BN> fb;
+  fa.init(lane);
+  fb.init(lane);
 
   f32x16_t acc[TN][TM];
 #pragma unroll
@@ -213,63 +276,90 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_mfma_kernel(GemmBatch batch
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[j][i][e] = 0.0f;
 
+  // Software pipeline over an NS-stage LDS ring.  Fragments of K sub-step
+  // ks + 1 are read while the MFMAs of sub-step ks run (two register sets).
+  // The one barrier per K stage sits before the last sub-step: by then every
+  // wave has read all fragments of stage kt, so the loads of stage kt + NS may
+  // overwrite it, and the first fragments of stage kt + 1 are read while the
+  // last MFMAs of stage kt run.  Before the barrier each wave waits only for
+  // its own loads of stage kt + 1 (later stages stay in flight).  Scheduling
+  // fences keep each sub-step's reads ahead of its MFMAs.
+  constexpr int LPT = TileLoader<A_T, BM, NW>::kInst + TileLoader<B_T, BN, NW>::kInst;  // loads per stage
   const int KT = p.K / kBK;
-  stage_load<A_T, BM, NT>(ra, A, p.lda, m0, p.M, 0, tid);
-  stage_load<B_T, BN, NT>(rb, B, p.ldb, n0, p.N, 0, tid);
-  stage_store<A_T, BM, NT>(ra, As, tid);
-  stage_store<B_T, BN, NT>(rb, Bs, tid);
-  __syncthreads();
-
-  const int arow = wm * TM * 32 + (lane & 31);
-  const int brow = wn * TN * 32 + (lane & 31);
-  const int kofs = (lane >> 5) * 8;
-
-  for (int kt = 0; kt < KT; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < KT) {
-      stage_load<A_T, BM, NT>(ra, A, p.lda, m0, p.M, (kt + 1) * kBK, tid);
-      stage_load<B_T, BN, NT>(rb, B, p.ldb, n0, p.N, (kt + 1) * kBK, tid);
-    }
-    const bf16_t* as = As + buf * BM * kLDK;
-    const bf16_t* bs = Bs + buf * BN * kLDK;
+  bf16x8_t a0[TM], a1[TM], b0[TN], b1[TN];  // two fragment register sets
+  auto read_frags = [&](const char* st, int ks, bf16x8_t (&a)[TM], bf16x8_t (&b)[TN]) {
 #pragma unroll
-    for (int ks = 0; ks < kBK / 16; ++ks) {
-      bf16x8_t af[TM], bfr[TN];
+    for (int i = 0; i < TM; ++i) a[i] = fa.read(st, wm * WTM + i * 32, ks);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) b[j] = fb.read(st + A_BYTES, wn * WTN + j * 32, ks);
+  };
+  auto mfmas = [&](const bf16x8_t (&a)[TM], const bf16x8_t (&b)[TN]) {
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int i = 0; i < TM; ++i)
-        af[i] = *reinterpret_cast<const bf16x8_t*>(as + (arow + i * 32) * kLDK + ks * 16 + kofs);
+        acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[j], a[i], acc[j][i], 0, 0, 0);
+  };
+  auto issue = [&](int stage) {
+    char* st = smem + stage * STAGE;
+    la.issue(ra, st, wave);
+    lb.issue(rb, st + A_BYTES, wave);
+  };
+  // reads of (st, ks) into set n, then the MFMAs of set c
+  auto step = [&](const char* st, int ks, bf16x8_t (&na)[TM], bf16x8_t (&nb)[TN], const bf16x8_t (&ca)[TM],
+                  const bf16x8_t (&cb)[TN]) {
+    read_frags(st, ks, na, nb);
+    __builtin_amdgcn_sched_barrier(0);
+    mfmas(ca, cb);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
 #pragma unroll
-      for (int j = 0; j < TN; ++j)
-        bfr[j] = *reinterpret_cast<const bf16x8_t*>(bs + (brow + j * 32) * kLDK + ks * 16 + kofs);
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-          acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[j][i], 0, 0, 0);
-    }
-    if (kt + 1 < KT) {
-      stage_store<A_T, BM, NT>(ra, As + (buf ^ 1) * BM * kLDK, tid);
-      stage_store<B_T, BN, NT>(rb, Bs + (buf ^ 1) * BN * kLDK, tid);
-    }
-    __syncthreads();
+  for (int s = 0; s < NS; ++s)
+    if (s < KT) issue(s);
+  if (KT >= NS) wait_vm_barrier<(NS - 1) * LPT>();
+  else wait_vm_barrier<0>();
+  read_frags(smem, 0, a0, b0);
+  __builtin_amdgcn_sched_barrier(0);
+
+  static_assert(kBK / 16 == 4, "the sub-step sequence below assumes four sub-steps per stage");
+  for (int kt = 0; kt < KT - 1; ++kt) {
+    const int cur = kt % NS;
+    const char* st = smem + cur * STAGE;
+    step(st, 1, a1, b1, a0, b0);
+    step(st, 2, a0, b0, a1, b1);
+    step(st, 3, a1, b1, a0, b0);
+    if (kt + NS - 1 < KT) wait_vm_barrier<(NS - 2) * LPT>();
+    else wait_vm_barrier<0>();
+    if (kt + NS < KT) issue(cur);
+    step(smem + ((kt + 1) % NS) * STAGE, 0, a0, b0, a1, b1);
+  }
+  {
+    const char* st = smem + ((KT - 1) % NS) * STAGE;
+    step(st, 1, a1, b1, a0, b0);
+    step(st, 2, a0, b0, a1, b1);
+    step(st, 3, a1, b1, a0, b0);
+    mfmas(a1, b1);
   }
 
-  // acc[j][i][r]: output row m = m0 + wm*TM*32 + i*32 + lane%32,
-  // column n = n0 + wn*TN*32 + j*32 + (r/4)*8 + (lane/32)*4 + r%4.
+  // acc[j][i][r]: output row m = m0 + wm*WTM + i*32 + lane%32,
+  // column n = n0 + wn*WTN + j*32 + (r/4)*8 + (lane/32)*4 + r%4.
 #pragma unroll
   for (int j = 0; j < TN; ++j)
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
-      const int m = m0 + wm * TM * 32 + i * 32 + (lane & 31);
+      const int m = m0 + wm * WTM + i * 32 + (lane & 31);
       if (m >= p.M) continue;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int n = n0 + wn * TN * 32 + j * 32 + g * 8 + (lane >> 5) * 4;
+        const int n = n0 + wn * WTN + j * 32 + g * 8 + (lane >> 5) * 4;
         if (n < p.N) {
           float v[4] = {acc[j][i][4 * g], acc[j][i][4 * g + 1], acc[j][i][4 * g + 2], acc[j][i][4 * g + 3]};
           epilogue4<bf16_t, EPI>(p, m, n, v);
         }
       }
+      // one output block at a time (keeps the accumulators in place)
+      __builtin_amdgcn_sched_barrier(0);
     }
 }
 
@@ -328,7 +418,7 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(GemmBatch batch) {
 // ---------------------------------------------------------------------------
 // Host dispatch
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int WM, int WN, bool AT, bool BT, int EPI>
+template <int BM, int BN, int WM, int WN, int NS, bool AT, bool BT, int EPI>
 static hipError_t run_mfma(GemmBatch& batch, hipStream_t stream) {
   int tiles = 0;
   for (int i = 0; i < batch.n_probs; ++i) {
@@ -337,8 +427,9 @@ static hipError_t run_mfma(GemmBatch& batch, hipStream_t stream) {
   }
   for (int i = batch.n_probs; i <= kMaxGroup; ++i) batch.tile_start[i] = tiles;
   if (tiles == 0) return hipSuccess;
-  constexpr size_t lds = (size_t)2 * (BM + BN) * kLDK * sizeof(bf16_t);
-  auto kern = gemm_mfma_kernel<BM, BN, WM, WN, AT, BT, EPI>;
+  constexpr size_t lds = (size_t)NS * (BM + BN) * 128;
+  static_assert(lds <= 160 * 1024, "LDS budget");
+  auto kern = gemm_mfma_kernel<BM, BN, WM, WN, NS, AT, BT, EPI>;
   static bool attr_set = false;  // per instantiation
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -363,13 +454,52 @@ static hipError_t run_f32(GemmBatch& batch, hipStream_t stream) {
   return hipGetLastError();
 }
 
+// Tile shapes of the bf16 kernel: BM x BN with WM x WN waves and NS LDS stages.
+enum TileCfg {
+  TILE_AUTO = 0,
+  TILE_256x256_W4_S2 = 1,  // 2x2 waves of 128x128
+  TILE_256x128_W4_S3 = 2,  // 2x2 waves of 128x64
+  TILE_128x256_W4_S3 = 3,  // 2x2 waves of 64x128
+  TILE_128x128_W4_S2 = 4,  // 2x2 waves of 64x64
+  TILE_128x128_W4_S3 = 5,
+  TILE_128x128_W4_S4 = 6,
+  TILE_256x256_W8_S2 = 7,  // 2x4 waves of 128x64
+  TILE_256x128_W8_S3 = 8,  // 4x2 waves of 64x64
+  TILE_COUNT = 9
+};
+static int g_tile_override = TILE_AUTO;
+
+static long long tile_count(const GemmBatch& b, int bm, int bn) {
+  long long t = 0;
+  for (int i = 0; i < b.n_probs; ++i) t += (long long)((b.p[i].M + bm - 1) / bm) * ((b.p[i].N + bn - 1) / bn);
+  return t;
+}
+
+// Tile choice (measured on MI355X with random bf16 data): long reductions
+// (K >= 4096, e.g. the weight gradients over a whole micro-batch) with enough
+// 256 x 256 tiles to occupy the chip run best as 256 x 256 tiles on 8 waves;
+// everything else (the per-sub-micro-batch layers, K <= 3072) as 128 x 128
+// tiles on 4 waves, two or three workgroups per CU.
+static int choose_tile(const GemmBatch& b) {
+  if (g_tile_override != TILE_AUTO) return g_tile_override;
+  int kmin = b.p[0].K;
+  for (int i = 1; i < b.n_probs; ++i) kmin = b.p[i].K < kmin ? b.p[i].K : kmin;
+  if (kmin >= 4096 && tile_count(b, 256, 256) >= 128) return TILE_256x256_W8_S2;
+  return TILE_128x128_W4_S2;
+}
+
 template <bool AT, bool BT, int EPI>
 static hipError_t run_bf16(GemmBatch& batch, hipStream_t stream) {
-  long long big_tiles = 0;
-  for (int i = 0; i < batch.n_probs; ++i)
-    big_tiles += (long long)((batch.p[i].M + 255) / 256) * ((batch.p[i].N + 255) / 256);
-  if (big_tiles >= 240) return run_mfma<256, 256, 2, 2, AT, BT, EPI>(batch, stream);
-  return run_mfma<128, 128, 2, 2, AT, BT, EPI>(batch, stream);
+  switch (choose_tile(batch)) {
+    case TILE_256x256_W4_S2: return run_mfma<256, 256, 2, 2, 2, AT, BT, EPI>(batch, stream);
+    case TILE_256x128_W4_S3: return run_mfma<256, 128, 2, 2, 3, AT, BT, EPI>(batch, stream);
+    case TILE_128x256_W4_S3: return run_mfma<128, 256, 2, 2, 3, AT, BT, EPI>(batch, stream);
+    case TILE_128x128_W4_S3: return run_mfma<128, 128, 2, 2, 3, AT, BT, EPI>(batch, stream);
+    case TILE_128x128_W4_S4: return run_mfma<128, 128, 2, 2, 4, AT, BT, EPI>(batch, stream);
+    case TILE_256x256_W8_S2: return run_mfma<256, 256, 2, 4, 2, AT, BT, EPI>(batch, stream);
+    case TILE_256x128_W8_S3: return run_mfma<256, 128, 4, 2, 3, AT, BT, EPI>(batch, stream);
+    default: return run_mfma<128, 128, 2, 2, 2, AT, BT, EPI>(batch, stream);
+  }
 }
 
 template <bool AT, bool BT>
@@ -393,6 +523,14 @@ static hipError_t dispatch_epi(int dtype, int epi, GemmBatch& batch, hipStream_t
 hipError_t launch_gemm(int dtype, bool a_t, bool b_t, int epi, const GemmProblem* probs, int n_probs,
                        hipStream_t stream) {
   if (n_probs < 1 || n_probs > kMaxGroup) return hipErrorInvalidValue;
+  // The bf16 kernel addresses each operand with 32-bit byte offsets, including
+  // the rows of a partial edge tile.
+  for (int i = 0; i < n_probs; ++i) {
+    const GemmProblem& q = probs[i];
+    const long long ea = (long long)(a_t ? q.K : q.M + 256) * q.lda + (a_t ? q.M + 256 : q.K);
+    const long long eb = (long long)(b_t ? q.K : q.N + 256) * q.ldb + (b_t ? q.N + 256 : q.K);
+    if (dtype == DT_BF16 && (2 * ea >= (1LL << 31) || 2 * eb >= (1LL << 31))) return hipErrorInvalidValue;
+  }
   GemmBatch batch;
   for (int i = 0; i < n_probs; ++i) batch.p[i] = probs[i];
   batch.n_probs = n_probs;
@@ -403,3 +541,10 @@ hipError_t launch_gemm(int dtype, bool a_t, bool b_t, int epi, const GemmProblem
 }
 
 }  // namespace merak
+
+extern "C" int merak_gemm_tile_override(int cfg) {
+  if (cfg < merak::TILE_AUTO || cfg >= merak::TILE_COUNT) return -1;
+  const int prev = merak::g_tile_override;
+  merak::g_tile_override = cfg;
+  return prev;
+}

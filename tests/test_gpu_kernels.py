@@ -170,3 +170,25 @@ def test_attention_fwd_bwd(dtype, d, seq, batch, heads):
     assert rel_err(g[:, :, 0], dq) < tol
     assert rel_err(g[:, :, 1], dk) < tol
     assert rel_err(g[:, :, 2], dv) < tol
+
+
+@pytest.mark.parametrize("cfg", list(range(1, 9)))
+@pytest.mark.parametrize("a_t,b_t", [(0, 0), (0, 1), (1, 1), (1, 0)])
+def test_gemm_every_tile_shape(cfg, a_t, b_t):
+    """Each tile shape of the bf16 kernel on a ragged problem (M, N not
+    multiples of 128 or 256; K spans 5 stages), fp32 output so the check is
+    tight."""
+    torch = need_gpu()
+    M, N, K = 320, 448, 320
+    print(f"[gemm tile {cfg}] a_t={a_t} b_t={b_t}", flush=True)
+    a_p, a = _rand((K, M) if a_t else (M, K), "bf16", 21)
+    b_p, b = _rand((K, N) if b_t else (N, K), "bf16", 22)
+    ref = (a.T if a_t else a) @ (b if b_t else b.T)
+    c32 = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    prev = B.gemm_tile_override(cfg)
+    try:
+        B.gemm(_dev(a_p), _dev(b_p), c32, M, N, K, a_trans=a_t, b_trans=b_t, epilogue=B.EPI_F32, dtype=B.BF16)
+        torch.cuda.synchronize()
+    finally:
+        B.gemm_tile_override(prev)
+    assert rel_err(c32.cpu().numpy(), ref) < 2e-5
