@@ -35,7 +35,9 @@ namespace merak {
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
-typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef short s16x8_t __attribute__((ext_vector_type(8)));
+#define MERAK_LDS __attribute__((address_space(3)))
 
 __device__ __forceinline__ bf16x8_t cvt8(const f32x16_t& a, int base) {
   bf16x8_t r;
@@ -44,85 +46,104 @@ __device__ __forceinline__ bf16x8_t cvt8(const f32x16_t& a, int base) {
   return r;
 }
 
-// Operand of 8 elements from a transposed LDS tile (rows = MFMA i index, row
-// contiguous along the 16-deep group): elements e=0..3 at cols kb+4*hf+0..3,
-// e=4..7 at cols kb+8+4*hf+0..3.
-__device__ __forceinline__ bf16x8_t frag_t(const bf16_t* row, int kb, int hf) {
-  const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(row + kb + 4 * hf);
-  const u32x2_t hi = *reinterpret_cast<const u32x2_t*>(row + kb + 8 + 4 * hf);
-  u32x4_t v = {lo[0], lo[1], hi[0], hi[1]};
+// A [64 rows][D] bf16 tile in LDS with rows padded to LD elements: 16-byte
+// reads of 16 consecutive rows hit distinct banks, the transposing reads of 4
+// consecutive rows at most two-way.  LD * 2 is a multiple of 16, so the tile is
+// exactly CPR wave-instructions of 16-byte-per-lane direct loads.
+template <int D>
+struct AttnTile {
+  static constexpr int LD = D == 128 ? D + 24 : D + 8;
+  static constexpr int CPR = LD / 8;         // 16-byte chunks per padded row
+  static constexpr int DC = D / 8;           // data chunks per row
+  static constexpr int BYTES = 64 * LD * 2;  // = CPR * 1024
+};
+
+// One wave copies rows 0..63 of `src` (row stride gs elements) into the padded
+// tile at `lds` with loads that write LDS directly (lane i of instruction q
+// fills chunk 64 q + i; padding chunks re-read a data chunk).
+template <int D>
+__device__ __forceinline__ void wave_tile_load(char* lds, const bf16_t* src, size_t gs, int lane) {
+  using TT = AttnTile<D>;
+#pragma unroll
+  for (int q = 0; q < TT::CPR; ++q) {
+    const int c = q * 64 + lane;
+    const int row = c / TT::CPR, ch = c % TT::CPR;
+    const bf16_t* g = src + (size_t)row * gs + (ch < TT::DC ? ch : 0) * 8;
+    __builtin_amdgcn_global_load_lds(g, (MERAK_LDS void*)(lds + q * 1024), 16, 0, 0);
+  }
+}
+
+// 64 floats (one per lane) into LDS with a direct load.
+__device__ __forceinline__ void wave_vec_load(char* lds, const float* src, int lane) {
+  __builtin_amdgcn_global_load_lds(src + lane, (MERAK_LDS void*)lds, 4, 0, 0);
+}
+
+// 8 consecutive elements of row `row` from column `col` of a padded tile.
+template <int LD>
+__device__ __forceinline__ bf16x8_t frag_row(const char* tile, int row, int col) {
+  return *reinterpret_cast<const bf16x8_t*>(tile + (row * LD + col) * 2);
+}
+
+// MFMA operand of X^T taken from a natural tile X[row][col]: lane l gets
+// column col0 + l % 32 and rows kb + 4 (l / 32) + 0..3 (elements 0..3) and
+// kb + 8 + 4 (l / 32) + 0..3 (elements 4..7), the key order of an accumulator
+// reused as the 16-deep operand.  Two transposing LDS reads: in each 16-lane
+// group, lane j fetches 4 columns of row (j / 4) and lane i receives column i of
+// the 4 rows.
+template <int LD>
+__device__ __forceinline__ bf16x8_t frag_tr(const char* tile, int kb, int col0, int lane) {
+  const int row = kb + (lane >> 5) * 4 + ((lane & 15) >> 2);
+  const int col = col0 + ((lane >> 4) & 1) * 16 + (lane & 3) * 4;
+  const char* p = tile + (row * LD + col) * 2;
+  const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((MERAK_LDS s16x4_t*)p);
+  const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((MERAK_LDS s16x4_t*)(p + 8 * LD * 2));
+  const s16x8_t v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
   return __builtin_bit_cast(bf16x8_t, v);
 }
 
 __device__ __forceinline__ bf16x8_t frag_kc(const bf16_t* p) { return *reinterpret_cast<const bf16x8_t*>(p); }
 
-// Copy a [64 rows][D] tile (global row stride gs) into LDS [64][LD] (LD % 8 == 0).
-template <int D, int LD, int NT>
-__device__ __forceinline__ void tile_to_lds(bf16_t* dst, const bf16_t* src, size_t gs, int tid) {
-  constexpr int CPR = D / 8;
-  for (int c = tid; c < 64 * CPR; c += NT) {
-    const int row = c / CPR, ch = c % CPR;
-    *reinterpret_cast<u32x4_t*>(dst + row * LD + ch * 8) =
-        *reinterpret_cast<const u32x4_t*>(src + (size_t)row * gs + ch * 8);
-  }
-}
-
-// Copy a [64 rows][D] tile transposed into LDS [D][LDT] (LDT % 4 == 0):
-// 8x8 blocks through registers, written as two 8-byte halves.
-template <int D, int LDT, int NT>
-__device__ __forceinline__ void tile_to_lds_t(bf16_t* dst, const bf16_t* src, size_t gs, int tid) {
-  constexpr int CPR = D / 8;
-  for (int c = tid; c < 8 * CPR; c += NT) {
-    const int dc = c % CPR, rg = c / CPR;
-    u32x4_t r[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-      r[j] = *reinterpret_cast<const u32x4_t*>(src + (size_t)(rg * 8 + j) * gs + dc * 8);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      uint32_t o[4];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const uint32_t lo = r[2 * q][e >> 1], hi = r[2 * q + 1][e >> 1];
-        o[q] = (e & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
-      }
-      bf16_t* d = dst + (dc * 8 + e) * LDT + rg * 8;
-      *reinterpret_cast<u32x2_t*>(d) = u32x2_t{o[0], o[1]};
-      *reinterpret_cast<u32x2_t*>(d + 4) = u32x2_t{o[2], o[3]};
-    }
-  }
-}
+// Dynamic LDS of the bf16 kernels: two stages of four tiles.
+template <int D>
+constexpr size_t attn_lds_bytes() { return (size_t)8 * AttnTile<D>::BYTES; }
 
 // ---------------------------------------------------------------------------
-// bf16 forward
+// bf16 forward.  A workgroup owns 64 query rows of one (batch, head); wave w
+// takes the 32 rows of group w % 2 against the even (w < 2) or odd 64-key
+// blocks, and the two halves are merged at the end (online-softmax merge).
+// Each stage holds the K and V tiles of two key blocks.
 // ---------------------------------------------------------------------------
-template <int D, int NW>
-__global__ void __launch_bounds__(NW * 64) attn_fwd_bf16(int S, int H, const bf16_t* __restrict__ qkv,
-                                                         bf16_t* __restrict__ o, float* __restrict__ lse,
-                                                         float scale_log2) {
-  constexpr int NT = NW * 64;
-  constexpr int LDK = D + 8;
-  constexpr int LDV = 64 + 4;
-  constexpr int KS = D / 16;
-  constexpr int DT = D / 32;
-  __shared__ __align__(16) bf16_t Ks[64 * LDK];
-  __shared__ __align__(16) bf16_t Vt[D * LDV];
+template <int D>
+__global__ void __launch_bounds__(256) attn_fwd_bf16(int S, int H, const bf16_t* __restrict__ qkv,
+                                                     bf16_t* __restrict__ o, float* __restrict__ lse,
+                                                     float scale_log2) {
+  using TT = AttnTile<D>;
+  constexpr int LD = TT::LD, KS = D / 16, DT = D / 32, TB = TT::BYTES;
+  extern __shared__ __align__(16) char smem[];  // [stage][K blk a, K blk b, V blk a, V blk b]
 
   const int b = blockIdx.z, hh = blockIdx.y;
-  const int qb = gridDim.x - 1 - blockIdx.x;  // longest rows first
-  const int qblk0 = qb * 32 * NW;
+  const int qt = gridDim.x - 1 - blockIdx.x;  // longest rows first
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, l32 = lane & 31, hf = lane >> 5;
-  const int q0 = qblk0 + wave * 32;
+  const int qg = wave & 1, kh = wave >> 1;
+  const int q0 = qt * 64 + qg * 32;
+  const int q = q0 + l32;
   const size_t rs = (size_t)3 * H * D;
   const bf16_t* base = qkv + (size_t)b * S * rs;
   const bf16_t* Qp = base + hh * D;
   const bf16_t* Kp = base + (size_t)H * D + hh * D;
   const bf16_t* Vp = base + (size_t)2 * H * D + hh * D;
 
-  const int myq = min(q0 + l32, S - 1);
   bf16x8_t qf[KS];
 #pragma unroll
-  for (int ks = 0; ks < KS; ++ks) qf[ks] = frag_kc(Qp + (size_t)myq * rs + ks * 16 + hf * 8);
+  for (int ks = 0; ks < KS; ++ks) qf[ks] = frag_kc(Qp + (size_t)q * rs + ks * 16 + hf * 8);
+
+  const int n_kb = qt + 1;  // key blocks 0..qt reach the tile's last row
+  const int n_it = (n_kb + 1) / 2;
+  auto load_stage = [&](int it, int stage) {  // wave w: tile w of the stage
+    const int blk = 2 * it + (wave & 1);
+    if (blk < n_kb)
+      wave_tile_load<D>(smem + (stage * 4 + wave) * TB, ((wave >> 1) ? Vp : Kp) + (size_t)blk * 64 * rs, rs, lane);
+  };
 
   f32x16_t oacc[DT];
 #pragma unroll
@@ -131,16 +152,14 @@ __global__ void __launch_bounds__(NW * 64) attn_fwd_bf16(int S, int H, const bf1
     for (int r = 0; r < 16; ++r) oacc[t][r] = 0.0f;
   float m = -INFINITY, l = 0.0f;
 
-  const int qlast_wg = min(qblk0 + 32 * NW, S) - 1;
-  const int n_kb = qlast_wg / 64 + 1;
-  const int q = q0 + l32;
-  for (int kb = 0; kb < n_kb; ++kb) {
-    const int k0 = kb * 64;
-    __syncthreads();
-    tile_to_lds<D, LDK, NT>(Ks, Kp + (size_t)k0 * rs, rs, tid);
-    tile_to_lds_t<D, LDV, NT>(Vt, Vp + (size_t)k0 * rs, rs, tid);
-    __syncthreads();
-    if (q0 >= S || k0 > q0 + 31) continue;
+  load_stage(0, 0);
+  for (int it = 0; it < n_it; ++it) {
+    __syncthreads();  // stage it landed; stage it+1 no longer read
+    if (it + 1 < n_it) load_stage(it + 1, (it + 1) & 1);
+    const int kb = 2 * it + kh, k0 = kb * 64;
+    if (kb >= n_kb || k0 > q0 + 31) continue;
+    const char* Kt = smem + ((it & 1) * 4 + kh) * TB;
+    const char* Vt = smem + ((it & 1) * 4 + 2 + kh) * TB;
 
     f32x16_t s[2];
 #pragma unroll
@@ -149,9 +168,10 @@ __global__ void __launch_bounds__(NW * 64) attn_fwd_bf16(int S, int H, const bf1
       for (int r = 0; r < 16; ++r) s[t][r] = 0.0f;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
-        s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_kc(Ks + (t * 32 + l32) * LDK + ks * 16 + hf * 8),
-                                                       qf[ks], s[t], 0, 0, 0);
+        s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_row<LD>(Kt, t * 32 + l32, ks * 16 + hf * 8), qf[ks],
+                                                       s[t], 0, 0, 0);
     }
+    // s[t][r]: key k0 + t*32 + (r/4)*8 + 4*hf + r%4, query q
     float mloc = -INFINITY;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
@@ -182,28 +202,47 @@ __global__ void __launch_bounds__(NW * 64) attn_fwd_bf16(int S, int H, const bf1
     bf16x8_t pb[4];
 #pragma unroll
     for (int g = 0; g < 4; ++g) pb[g] = cvt8(s[g >> 1], (g & 1) * 8);
+    // O^T[d][q] += V^T[d][key] P^T[key][q]
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
       for (int g = 0; g < 4; ++g)
-        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_t(Vt + (dt * 32 + l32) * LDV, g * 16, hf), pb[g],
-                                                           oacc[dt], 0, 0, 0);
+        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_tr<LD>(Vt, g * 16, dt * 32, lane), pb[g], oacc[dt],
+                                                           0, 0, 0);
   }
-  if (q0 >= S) return;
-  l += __shfl_xor(l, 32, 64);
-  const float inv = 1.0f / l;
-  if (q < S) {
-    bf16_t* orow = o + ((size_t)b * S + q) * H * D + hh * D;
+
+  // Merge the two key halves of each query group (partial m, l, O^T).
+  constexpr int XS = 2 + DT * 16;
+  float* xch = reinterpret_cast<float*>(smem) + (size_t)(qg * 64 + lane) * XS;
+  __syncthreads();
+  if (kh == 1) {
+    xch[0] = m;
+    xch[1] = l;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
+    for (int t = 0; t < DT; ++t)
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        float v[4] = {oacc[dt][4 * g] * inv, oacc[dt][4 * g + 1] * inv, oacc[dt][4 * g + 2] * inv,
-                      oacc[dt][4 * g + 3] * inv};
-        store4(orow + dt * 32 + g * 8 + hf * 4, v);
-      }
-    if (hf == 0) lse[((size_t)b * H + hh) * S + q] = (m + log2f(l)) * kLn2;
+      for (int r = 0; r < 16; ++r) xch[2 + t * 16 + r] = oacc[t][r];
   }
+  __syncthreads();
+  if (kh == 1) return;
+  const float m1 = xch[0], l1 = xch[1];
+  const float mt = fmaxf(m, m1);
+  const float a0 = exp2f(m - mt), a1 = exp2f(m1 - mt);
+  float lt = l * a0 + l1 * a1;
+  lt += __shfl_xor(lt, 32, 64);
+  const float inv = 1.0f / lt;
+  bf16_t* orow = o + ((size_t)b * S + q) * H * D + hh * D;
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      float v[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        v[e] = (oacc[dt][4 * g + e] * a0 + xch[2 + dt * 16 + 4 * g + e] * a1) * inv;
+      store4(orow + dt * 32 + g * 8 + hf * 4, v);
+    }
+  if (hf == 0) lse[((size_t)b * H + hh) * S + q] = (mt + log2f(lt)) * kLn2;
 }
 
 // ---------------------------------------------------------------------------
@@ -232,30 +271,30 @@ __global__ void __launch_bounds__(256) attn_delta_kernel(int B, int S, int H, co
 }
 
 // ---------------------------------------------------------------------------
-// bf16 backward: dK, dV (KV-parallel)
+// bf16 backward: dK, dV (KV-parallel).  A workgroup owns 64 keys of one
+// (batch, head); wave w takes the 32 keys of group w % 2 against the even
+// (w < 2) or odd 64-query blocks from the diagonal on, and the two partial sums
+// are added at the end.  Each stage holds the Q and dO tiles (and lse, delta)
+// of two query blocks.  P is rebuilt from lse.
 // ---------------------------------------------------------------------------
-template <int D, int NW>
-__global__ void __launch_bounds__(NW * 64) attn_bwd_dkdv_bf16(int S, int H, const bf16_t* __restrict__ qkv,
-                                                              const bf16_t* __restrict__ dout,
-                                                              const float* __restrict__ lse,
-                                                              const float* __restrict__ delta,
-                                                              bf16_t* __restrict__ dqkv, float scale_log2,
-                                                              float scale) {
-  constexpr int NT = NW * 64;
-  constexpr int LDK = D + 8;
-  constexpr int LDT = 64 + 4;
-  constexpr int KS = D / 16;
-  constexpr int DT = D / 32;
-  __shared__ __align__(16) bf16_t Qs[64 * LDK];
-  __shared__ __align__(16) bf16_t Qt[D * LDT];
-  __shared__ __align__(16) bf16_t dOs[64 * LDK];
-  __shared__ __align__(16) bf16_t dOt[D * LDT];
-  __shared__ float lse_s[64], del_s[64];
+template <int D>
+__global__ void __launch_bounds__(256) attn_bwd_dkdv_bf16(int S, int H, const bf16_t* __restrict__ qkv,
+                                                          const bf16_t* __restrict__ dout,
+                                                          const float* __restrict__ lse,
+                                                          const float* __restrict__ delta,
+                                                          bf16_t* __restrict__ dqkv, float scale_log2,
+                                                          float scale) {
+  using TT = AttnTile<D>;
+  constexpr int LD = TT::LD, KS = D / 16, DT = D / 32, TB = TT::BYTES;
+  extern __shared__ __align__(16) char smem[];  // [stage][Q a, Q b, dO a, dO b], then lse/delta
+  float* vecs = reinterpret_cast<float*>(smem + 8 * TB);  // [stage][lse a|b (128), delta a|b (128)]
 
   const int b = blockIdx.z, hh = blockIdx.y;
-  const int kblk0 = blockIdx.x * 32 * NW;  // early keys see the most queries: dispatched first
+  const int kt = blockIdx.x;  // early keys see the most queries: dispatched first
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, l32 = lane & 31, hf = lane >> 5;
-  const int kw0 = kblk0 + wave * 32;
+  const int kg = wave & 1, qh = wave >> 1;
+  const int kw0 = kt * 64 + kg * 32;
+  const int key = kw0 + l32;
   const size_t rs = (size_t)3 * H * D;
   const size_t ors = (size_t)H * D;
   const bf16_t* base = qkv + (size_t)b * S * rs;
@@ -266,12 +305,11 @@ __global__ void __launch_bounds__(NW * 64) attn_bwd_dkdv_bf16(int S, int H, cons
   const float* lse_p = lse + ((size_t)b * H + hh) * S;
   const float* del_p = delta + ((size_t)b * H + hh) * S;
 
-  const int mykey = min(kw0 + l32, S - 1);
   bf16x8_t kf[KS], vf[KS];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
-    kf[ks] = frag_kc(Kp + (size_t)mykey * rs + ks * 16 + hf * 8);
-    vf[ks] = frag_kc(Vp + (size_t)mykey * rs + ks * 16 + hf * 8);
+    kf[ks] = frag_kc(Kp + (size_t)key * rs + ks * 16 + hf * 8);
+    vf[ks] = frag_kc(Vp + (size_t)key * rs + ks * 16 + hf * 8);
   }
   f32x16_t dk[DT], dv[DT];
 #pragma unroll
@@ -279,19 +317,29 @@ __global__ void __launch_bounds__(NW * 64) attn_bwd_dkdv_bf16(int S, int H, cons
 #pragma unroll
     for (int r = 0; r < 16; ++r) dk[t][r] = dv[t][r] = 0.0f;
 
-  const int key = kw0 + l32;
-  for (int qs = (kblk0 / 64) * 64; qs < S; qs += 64) {
-    __syncthreads();
-    tile_to_lds<D, LDK, NT>(Qs, Qp + (size_t)qs * rs, rs, tid);
-    tile_to_lds_t<D, LDT, NT>(Qt, Qp + (size_t)qs * rs, rs, tid);
-    tile_to_lds<D, LDK, NT>(dOs, dOp + (size_t)qs * ors, ors, tid);
-    tile_to_lds_t<D, LDT, NT>(dOt, dOp + (size_t)qs * ors, ors, tid);
-    if (tid < 64) {
-      lse_s[tid] = lse_p[qs + tid] * kLog2e;
-      del_s[tid] = del_p[qs + tid];
+  const int n_qb = S / 64 - kt;  // query blocks kt .. S/64-1
+  const int n_it = (n_qb + 1) / 2;
+  auto load_stage = [&](int it, int stage) {
+    const int blk = kt + 2 * it + (wave & 1);
+    if (2 * it + (wave & 1) < n_qb) {
+      const bool is_do = (wave >> 1) != 0;
+      wave_tile_load<D>(smem + (stage * 4 + wave) * TB, is_do ? dOp + (size_t)blk * 64 * ors : Qp + (size_t)blk * 64 * rs,
+                        is_do ? ors : rs, lane);
+      float* v = vecs + stage * 256 + (wave & 1) * 64;
+      wave_vec_load(reinterpret_cast<char*>(v + (is_do ? 128 : 0)), (is_do ? del_p : lse_p) + (size_t)blk * 64, lane);
     }
+  };
+
+  load_stage(0, 0);
+  for (int it = 0; it < n_it; ++it) {
     __syncthreads();
-    if (kw0 >= S || qs + 63 < kw0) continue;
+    if (it + 1 < n_it) load_stage(it + 1, (it + 1) & 1);
+    const int qb = kt + 2 * it + qh, qs = qb * 64;
+    if (2 * it + qh >= n_qb || qs + 63 < kw0) continue;
+    const char* Qt = smem + ((it & 1) * 4 + qh) * TB;
+    const char* dOt = smem + ((it & 1) * 4 + 2 + qh) * TB;
+    const float* lse_s = vecs + (it & 1) * 256 + qh * 64;
+    const float* del_s = lse_s + 128;
 
     f32x16_t p[2], dp[2];
 #pragma unroll
@@ -300,10 +348,10 @@ __global__ void __launch_bounds__(NW * 64) attn_bwd_dkdv_bf16(int S, int H, cons
       for (int r = 0; r < 16; ++r) p[t][r] = dp[t][r] = 0.0f;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        p[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_kc(Qs + (t * 32 + l32) * LDK + ks * 16 + hf * 8),
-                                                       kf[ks], p[t], 0, 0, 0);
-        dp[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_kc(dOs + (t * 32 + l32) * LDK + ks * 16 + hf * 8),
-                                                        vf[ks], dp[t], 0, 0, 0);
+        p[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_row<LD>(Qt, t * 32 + l32, ks * 16 + hf * 8), kf[ks], p[t],
+                                                       0, 0, 0);
+        dp[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_row<LD>(dOt, t * 32 + l32, ks * 16 + hf * 8), vf[ks],
+                                                        dp[t], 0, 0, 0);
       }
     }
     // p[t][r]: query qs + t*32 + (r/4)*8 + 4*hf + r%4, key `key`.
@@ -312,7 +360,7 @@ __global__ void __launch_bounds__(NW * 64) attn_bwd_dkdv_bf16(int S, int H, cons
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int qi = t * 32 + (r >> 2) * 8 + hf * 4 + (r & 3);
-        const float pv = (key > qs + qi) ? 0.0f : exp2f(p[t][r] * scale_log2 - lse_s[qi]);
+        const float pv = (key > qs + qi) ? 0.0f : exp2f(p[t][r] * scale_log2 - lse_s[qi] * kLog2e);
         p[t][r] = pv;
         dp[t][r] = pv * (dp[t][r] - del_s[qi]);
       }
@@ -322,17 +370,33 @@ __global__ void __launch_bounds__(NW * 64) attn_bwd_dkdv_bf16(int S, int H, cons
       pb[g] = cvt8(p[g >> 1], (g & 1) * 8);
       sb[g] = cvt8(dp[g >> 1], (g & 1) * 8);
     }
+    // dV^T[d][key] += dO^T[d][q] P[q][key];  dK^T[d][key] += Q^T[d][q] dS[q][key]
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        dv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_t(dOt + (dt * 32 + l32) * LDT, g * 16, hf), pb[g],
-                                                         dv[dt], 0, 0, 0);
-        dk[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_t(Qt + (dt * 32 + l32) * LDT, g * 16, hf), sb[g],
-                                                         dk[dt], 0, 0, 0);
+        dv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_tr<LD>(dOt, g * 16, dt * 32, lane), pb[g], dv[dt], 0, 0,
+                                                         0);
+        dk[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_tr<LD>(Qt, g * 16, dt * 32, lane), sb[g], dk[dt], 0, 0,
+                                                         0);
       }
   }
-  if (kw0 >= S || key >= S) return;
+
+  // Add the two query halves.
+  constexpr int XS = 2 * DT * 16;
+  float* xch = reinterpret_cast<float*>(smem) + (size_t)(kg * 64 + lane) * XS;
+  __syncthreads();
+  if (qh == 1) {
+#pragma unroll
+    for (int t = 0; t < DT; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        xch[t * 16 + r] = dk[t][r];
+        xch[DT * 16 + t * 16 + r] = dv[t][r];
+      }
+  }
+  __syncthreads();
+  if (qh == 1) return;
   bf16_t* krow = dqkv + ((size_t)b * S + key) * rs + (size_t)H * D + hh * D;
   bf16_t* vrow = krow + (size_t)H * D;
 #pragma unroll
@@ -342,8 +406,8 @@ __global__ void __launch_bounds__(NW * 64) attn_bwd_dkdv_bf16(int S, int H, cons
       float a[4], c[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        a[e] = dk[dt][4 * g + e] * scale;
-        c[e] = dv[dt][4 * g + e];
+        a[e] = (dk[dt][4 * g + e] + xch[dt * 16 + 4 * g + e]) * scale;
+        c[e] = dv[dt][4 * g + e] + xch[DT * 16 + dt * 16 + 4 * g + e];
       }
       store4(krow + dt * 32 + g * 8 + hf * 4, a);
       store4(vrow + dt * 32 + g * 8 + hf * 4, c);
@@ -351,29 +415,26 @@ __global__ void __launch_bounds__(NW * 64) attn_bwd_dkdv_bf16(int S, int H, cons
 }
 
 // ---------------------------------------------------------------------------
-// bf16 backward: dQ (Q-parallel)
+// bf16 backward: dQ (Q-parallel), the forward's layout: 64 query rows per
+// workgroup, 2 query groups x 2 key halves, K and V tiles of two key blocks per
+// stage, partial dQ sums added at the end.
 // ---------------------------------------------------------------------------
-template <int D, int NW>
-__global__ void __launch_bounds__(NW * 64) attn_bwd_dq_bf16(int S, int H, const bf16_t* __restrict__ qkv,
-                                                            const bf16_t* __restrict__ dout,
-                                                            const float* __restrict__ lse,
-                                                            const float* __restrict__ delta,
-                                                            bf16_t* __restrict__ dqkv, float scale_log2,
-                                                            float scale) {
-  constexpr int NT = NW * 64;
-  constexpr int LDK = D + 8;
-  constexpr int LDT = 64 + 4;
-  constexpr int KS = D / 16;
-  constexpr int DT = D / 32;
-  __shared__ __align__(16) bf16_t Ks[64 * LDK];
-  __shared__ __align__(16) bf16_t Kt[D * LDT];
-  __shared__ __align__(16) bf16_t Vs[64 * LDK];
+template <int D>
+__global__ void __launch_bounds__(256) attn_bwd_dq_bf16(int S, int H, const bf16_t* __restrict__ qkv,
+                                                        const bf16_t* __restrict__ dout,
+                                                        const float* __restrict__ lse,
+                                                        const float* __restrict__ delta,
+                                                        bf16_t* __restrict__ dqkv, float scale_log2, float scale) {
+  using TT = AttnTile<D>;
+  constexpr int LD = TT::LD, KS = D / 16, DT = D / 32, TB = TT::BYTES;
+  extern __shared__ __align__(16) char smem[];
 
   const int b = blockIdx.z, hh = blockIdx.y;
-  const int qb = gridDim.x - 1 - blockIdx.x;
-  const int qblk0 = qb * 32 * NW;
+  const int qt = gridDim.x - 1 - blockIdx.x;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, l32 = lane & 31, hf = lane >> 5;
-  const int q0 = qblk0 + wave * 32;
+  const int qg = wave & 1, kh = wave >> 1;
+  const int q0 = qt * 64 + qg * 32;
+  const int q = q0 + l32;
   const size_t rs = (size_t)3 * H * D;
   const size_t ors = (size_t)H * D;
   const bf16_t* base = qkv + (size_t)b * S * rs;
@@ -382,32 +443,36 @@ __global__ void __launch_bounds__(NW * 64) attn_bwd_dq_bf16(int S, int H, const 
   const bf16_t* Vp = base + (size_t)2 * H * D + hh * D;
   const bf16_t* dOp = dout + (size_t)b * S * ors + hh * D;
 
-  const int myq = min(q0 + l32, S - 1);
   bf16x8_t qf[KS], of[KS];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
-    qf[ks] = frag_kc(Qp + (size_t)myq * rs + ks * 16 + hf * 8);
-    of[ks] = frag_kc(dOp + (size_t)myq * ors + ks * 16 + hf * 8);
+    qf[ks] = frag_kc(Qp + (size_t)q * rs + ks * 16 + hf * 8);
+    of[ks] = frag_kc(dOp + (size_t)q * ors + ks * 16 + hf * 8);
   }
-  const float lse2 = lse[((size_t)b * H + hh) * S + myq] * kLog2e;
-  const float del = delta[((size_t)b * H + hh) * S + myq];
+  const float lse2 = lse[((size_t)b * H + hh) * S + q] * kLog2e;
+  const float del = delta[((size_t)b * H + hh) * S + q];
   f32x16_t dq[DT];
 #pragma unroll
   for (int t = 0; t < DT; ++t)
 #pragma unroll
     for (int r = 0; r < 16; ++r) dq[t][r] = 0.0f;
 
-  const int qlast_wg = min(qblk0 + 32 * NW, S) - 1;
-  const int n_kb = qlast_wg / 64 + 1;
-  const int q = q0 + l32;
-  for (int kb = 0; kb < n_kb; ++kb) {
-    const int k0 = kb * 64;
+  const int n_kb = qt + 1;
+  const int n_it = (n_kb + 1) / 2;
+  auto load_stage = [&](int it, int stage) {
+    const int blk = 2 * it + (wave & 1);
+    if (blk < n_kb)
+      wave_tile_load<D>(smem + (stage * 4 + wave) * TB, ((wave >> 1) ? Vp : Kp) + (size_t)blk * 64 * rs, rs, lane);
+  };
+
+  load_stage(0, 0);
+  for (int it = 0; it < n_it; ++it) {
     __syncthreads();
-    tile_to_lds<D, LDK, NT>(Ks, Kp + (size_t)k0 * rs, rs, tid);
-    tile_to_lds_t<D, LDT, NT>(Kt, Kp + (size_t)k0 * rs, rs, tid);
-    tile_to_lds<D, LDK, NT>(Vs, Vp + (size_t)k0 * rs, rs, tid);
-    __syncthreads();
-    if (q0 >= S || k0 > q0 + 31) continue;
+    if (it + 1 < n_it) load_stage(it + 1, (it + 1) & 1);
+    const int kb = 2 * it + kh, k0 = kb * 64;
+    if (kb >= n_kb || k0 > q0 + 31) continue;
+    const char* Kt = smem + ((it & 1) * 4 + kh) * TB;
+    const char* Vt = smem + ((it & 1) * 4 + 2 + kh) * TB;
     f32x16_t p[2], dp[2];
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
@@ -415,31 +480,42 @@ __global__ void __launch_bounds__(NW * 64) attn_bwd_dq_bf16(int S, int H, const 
       for (int r = 0; r < 16; ++r) p[t][r] = dp[t][r] = 0.0f;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        p[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_kc(Ks + (t * 32 + l32) * LDK + ks * 16 + hf * 8),
-                                                       qf[ks], p[t], 0, 0, 0);
-        dp[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_kc(Vs + (t * 32 + l32) * LDK + ks * 16 + hf * 8),
-                                                        of[ks], dp[t], 0, 0, 0);
+        p[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_row<LD>(Kt, t * 32 + l32, ks * 16 + hf * 8), qf[ks], p[t],
+                                                       0, 0, 0);
+        dp[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_row<LD>(Vt, t * 32 + l32, ks * 16 + hf * 8), of[ks],
+                                                        dp[t], 0, 0, 0);
       }
     }
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int key = k0 + t * 32 + (r >> 2) * 8 + hf * 4 + (r & 3);
-        const float pv = key > q ? 0.0f : exp2f(p[t][r] * scale_log2 - lse2);
+        const int kk = k0 + t * 32 + (r >> 2) * 8 + hf * 4 + (r & 3);
+        const float pv = kk > q ? 0.0f : exp2f(p[t][r] * scale_log2 - lse2);
         dp[t][r] = pv * (dp[t][r] - del);
       }
     bf16x8_t sb[4];
 #pragma unroll
     for (int g = 0; g < 4; ++g) sb[g] = cvt8(dp[g >> 1], (g & 1) * 8);
+    // dQ^T[d][q] += K^T[d][key] dS^T[key][q]
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
       for (int g = 0; g < 4; ++g)
-        dq[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_t(Kt + (dt * 32 + l32) * LDT, g * 16, hf), sb[g],
-                                                         dq[dt], 0, 0, 0);
+        dq[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_tr<LD>(Kt, g * 16, dt * 32, lane), sb[g], dq[dt], 0, 0, 0);
   }
-  if (q0 >= S || q >= S) return;
+
+  constexpr int XS = DT * 16;
+  float* xch = reinterpret_cast<float*>(smem) + (size_t)(qg * 64 + lane) * XS;
+  __syncthreads();
+  if (kh == 1) {
+#pragma unroll
+    for (int t = 0; t < DT; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) xch[t * 16 + r] = dq[t][r];
+  }
+  __syncthreads();
+  if (kh == 1) return;
   bf16_t* qrow = dqkv + ((size_t)b * S + q) * rs + hh * D;
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt)
@@ -447,7 +523,7 @@ __global__ void __launch_bounds__(NW * 64) attn_bwd_dq_bf16(int S, int H, const 
     for (int g = 0; g < 4; ++g) {
       float a[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) a[e] = dq[dt][4 * g + e] * scale;
+      for (int e = 0; e < 4; ++e) a[e] = (dq[dt][4 * g + e] + xch[dt * 16 + 4 * g + e]) * scale;
       store4(qrow + dt * 32 + g * 8 + hf * 4, a);
     }
 }
@@ -569,16 +645,27 @@ __global__ void __launch_bounds__(128) attn_bwd_dkdv_f32(int B, int S, int H, co
 // ---------------------------------------------------------------------------
 // Host launchers
 // ---------------------------------------------------------------------------
-constexpr int kAttnWaves = 4;
+// Allow a kernel's dynamic LDS beyond the default limit (once per instantiation).
+template <typename K>
+static hipError_t allow_lds(K kern, size_t bytes, bool& done) {
+  if (done) return hipSuccess;
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     (int)bytes);
+  if (e == hipSuccess) done = true;
+  return e;
+}
 
 template <int D>
 static hipError_t fwd_d(int dtype, int B, int S, int H, const void* qkv, void* o, float* lse, hipStream_t st) {
   const float scale = 1.0f / sqrtf((float)D);
   if (dtype == DT_BF16) {
-    constexpr int QB = 32 * kAttnWaves;
-    dim3 grid((S + QB - 1) / QB, H, B);
-    hipLaunchKernelGGL((attn_fwd_bf16<D, kAttnWaves>), grid, dim3(64 * kAttnWaves), 0, st, S, H,
-                       (const bf16_t*)qkv, (bf16_t*)o, lse, scale * kLog2e);
+    constexpr size_t lds = attn_lds_bytes<D>();
+    static bool ok = false;
+    hipError_t e = allow_lds(attn_fwd_bf16<D>, lds, ok);
+    if (e != hipSuccess) return e;
+    dim3 grid(S / 64, H, B);
+    hipLaunchKernelGGL((attn_fwd_bf16<D>), grid, dim3(256), lds, st, S, H, (const bf16_t*)qkv, (bf16_t*)o, lse,
+                       scale * kLog2e);
   } else {
     dim3 grid((B * H * S + 127) / 128);
     hipLaunchKernelGGL((attn_fwd_f32<D>), grid, dim3(128), 0, st, B, S, H, (const float*)qkv, (float*)o, lse,
@@ -593,14 +680,20 @@ static hipError_t bwd_d(int dtype, int B, int S, int H, const void* qkv, const v
   const float scale = 1.0f / sqrtf((float)D);
   const int rows = B * S * H;
   if (dtype == DT_BF16) {
+    constexpr size_t lds_q = attn_lds_bytes<D>();
+    constexpr size_t lds_k = attn_lds_bytes<D>() + 2 * 256 * sizeof(float);
+    static_assert(lds_k <= 160 * 1024, "LDS budget");
+    static bool ok_k = false, ok_q = false;
+    hipError_t e = allow_lds(attn_bwd_dkdv_bf16<D>, lds_k, ok_k);
+    if (e == hipSuccess) e = allow_lds(attn_bwd_dq_bf16<D>, lds_q, ok_q);
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL((attn_delta_kernel<bf16_t, D>), dim3((rows + 255) / 256), dim3(256), 0, st, B, S, H,
                        (const bf16_t*)o, (const bf16_t*)dout, delta);
-    constexpr int BLK = 32 * kAttnWaves;
-    dim3 grid((S + BLK - 1) / BLK, H, B);
-    hipLaunchKernelGGL((attn_bwd_dkdv_bf16<D, kAttnWaves>), grid, dim3(64 * kAttnWaves), 0, st, S, H,
-                       (const bf16_t*)qkv, (const bf16_t*)dout, lse, delta, (bf16_t*)dqkv, scale * kLog2e, scale);
-    hipLaunchKernelGGL((attn_bwd_dq_bf16<D, kAttnWaves>), grid, dim3(64 * kAttnWaves), 0, st, S, H,
-                       (const bf16_t*)qkv, (const bf16_t*)dout, lse, delta, (bf16_t*)dqkv, scale * kLog2e, scale);
+    dim3 grid(S / 64, H, B);
+    hipLaunchKernelGGL((attn_bwd_dkdv_bf16<D>), grid, dim3(256), lds_k, st, S, H, (const bf16_t*)qkv,
+                       (const bf16_t*)dout, lse, delta, (bf16_t*)dqkv, scale * kLog2e, scale);
+    hipLaunchKernelGGL((attn_bwd_dq_bf16<D>), grid, dim3(256), lds_q, st, S, H, (const bf16_t*)qkv,
+                       (const bf16_t*)dout, lse, delta, (bf16_t*)dqkv, scale * kLog2e, scale);
   } else {
     hipLaunchKernelGGL((attn_delta_kernel<float, D>), dim3((rows + 255) / 256), dim3(256), 0, st, B, S, H,
                        (const float*)o, (const float*)dout, delta);
