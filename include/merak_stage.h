@@ -234,9 +234,9 @@ int merak_gemm(int dtype, int a_trans, int b_trans, int epilogue, int M, int N, 
                const void* resid, void* aux, int accumulate, void* stream);
 
 /* Tile-shape override of the bf16 GEMM kernel, for tests and tuning:
- * 0 restores the built-in choice, 1..8 force one shape (256x256/4 waves/2
+ * 0 restores the built-in choice, 1..9 force one shape (256x256/4 waves/2
  * stages, 256x128/4/3, 128x256/4/3, 128x128/4/2, 128x128/4/3, 128x128/4/4,
- * 256x256/8/2, 256x128/8/3).  Process-wide; returns the previous value, or -1
+ * 256x256/8/2, 256x128/8/3, 128x192/4/2).  Process-wide; returns the previous value, or -1
  * for an out-of-range cfg (nothing changed).  Host-only, not thread-safe. */
 int merak_gemm_tile_override(int cfg);
 

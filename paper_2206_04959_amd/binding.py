@@ -239,7 +239,7 @@ def gemm(a, b, c, M, N, K, a_trans=False, b_trans=False, epilogue=EPI_STORE, bia
 
 
 def gemm_tile_override(cfg: int) -> int:
-    """Force a bf16 GEMM tile shape (1..8) or restore the built-in choice (0);
+    """Force a bf16 GEMM tile shape (1..9) or restore the built-in choice (0);
     returns the previous setting."""
     prev = int(lib().merak_gemm_tile_override(int(cfg)))
     if prev < 0:

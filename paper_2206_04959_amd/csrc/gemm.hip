@@ -105,8 +105,9 @@ __device__ __forceinline__ GemmProblem select_problem(const GemmBatch& b, int bi
 //     slot c ^ ((r >> 1) & 7), so the 16 rows read by one 256-byte pass of a
 //     fragment read land in distinct banks (gfx950 LDS: 64 banks of 4 bytes);
 //   MN-contiguous operand: [64 k][R]; chunk c of k-row k is stored in slot
-//     c ^ (4 * (k & 3)), so the four k-rows of a transposing read pass are
-//     spread over the 256-byte bank space.
+//     (c + 4 * (k & 3)) mod (R / 8), so the four k-rows of a transposing read
+//     pass land in distinct quarters of the 256-byte bank space (R = 128, 192
+//     or 256).
 // Tiles move global -> LDS with buffer loads that write LDS directly (no VGPR
 // staging); each wave instruction fills 1 KiB of LDS, lane i writing bytes
 // [16 i, 16 i + 16), and the swizzle is applied by choosing which global
@@ -138,7 +139,7 @@ template <bool TRANS, int R, int NW>
 struct TileLoader {
   static constexpr int kInst = R / 8 / NW;
   static_assert(R / 8 % NW == 0, "tile rows must split evenly over the waves");
-  static_assert(!TRANS || R == 128 || R == 256, "MN-contiguous tiles must be 128 or 256 wide");
+  static_assert(!TRANS || (R % 32 == 0 && R >= 128), "MN-contiguous tiles: width a multiple of 32, at least 128");
   uint32_t voff[kInst];
   uint32_t step;  // bytes to advance per K stage
 
@@ -150,10 +151,10 @@ struct TileLoader {
         const int chunk = (lane & 7) ^ ((row >> 1) & 7);
         voff[q] = (uint32_t)((r0 + row) * ld + chunk * 8) * 2u;
       } else {
-        constexpr int CPR = R / 8;     // 16-byte chunks per k-row
-        constexpr int KPI = 64 / CPR;  // k-rows per wave instruction
-        const int kr = (q * NW + wave) * KPI + lane / CPR;
-        const int chunk = (lane % CPR) ^ ((kr & 3) << 2);
+        constexpr int CPR = R / 8;  // 16-byte chunks per k-row
+        const int g = (q * NW + wave) * 64 + lane;  // chunk index within the stage
+        const int kr = g / CPR, slot = g % CPR;
+        const int chunk = (slot + CPR - 4 * (kr & 3)) % CPR;  // chunk stored in this slot
         voff[q] = (uint32_t)(kr * ld + r0 + chunk * 8) * 2u;
       }
     }
@@ -196,7 +197,7 @@ struct FragReader {
     } else {
       const int b = lane >> 4, j = lane & 15;
       lane_off = ((b >> 1) * 8 + (j >> 2)) * (2 * R) + ((b & 1) * 2 + ((j >> 1) & 1)) * 16 + (j & 1) * 8;
-      key = (j >> 2) << 2;
+      key = (j >> 2) << 2;  // slot rotation of this lane's k-row (k & 3 = j / 4)
     }
   }
 
@@ -205,7 +206,8 @@ struct FragReader {
       const char* p = lds + row0 * 128 + lane_off + (((2 * ks) ^ key) << 4);
       return *reinterpret_cast<const bf16x8_t*>(p);
     } else {
-      const char* p = lds + ks * 16 * (2 * R) + ((((row0 >> 3)) ^ key) << 4) + lane_off;
+      constexpr int CPR = R / 8;
+      const char* p = lds + ks * 16 * (2 * R) + ((((row0 >> 3) + key) % CPR) << 4) + lane_off;
       s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((MERAK_LDS s16x4_t*)(p));
       s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((MERAK_LDS s16x4_t*)(p + 4 * (2 * R)));
       s16x4_t v01 = lo, v23 = hi;
@@ -465,7 +467,8 @@ enum TileCfg {
   TILE_128x128_W4_S4 = 6,
   TILE_256x256_W8_S2 = 7,  // 2x4 waves of 128x64
   TILE_256x128_W8_S3 = 8,  // 4x2 waves of 64x64
-  TILE_COUNT = 9
+  TILE_128x192_W4_S2 = 9,  // 2x2 waves of 64x96
+  TILE_COUNT = 10
 };
 static int g_tile_override = TILE_AUTO;
 
@@ -475,16 +478,19 @@ static long long tile_count(const GemmBatch& b, int bm, int bn) {
   return t;
 }
 
-// Tile choice (measured on MI355X with random bf16 data): long reductions
-// (K >= 4096, e.g. the weight gradients over a whole micro-batch) with enough
-// 256 x 256 tiles to occupy the chip run best as 256 x 256 tiles on 8 waves;
-// everything else (the per-sub-micro-batch layers, K <= 3072) as 128 x 128
-// tiles on 4 waves, two or three workgroups per CU.
+// Tile choice (measured on MI355X with random bf16 data).  Long reductions
+// (K >= 4096: the weight gradients over a whole micro-batch): 256 x 256 tiles
+// on 8 waves when there are enough of them to fill the chip twice, else
+// 128 x 192 tiles (64 x 96 per wave, two workgroups per CU).  Everything else
+// (the per-sub-micro-batch layers, K <= 3072): 128 x 128 tiles on 4 waves.
 static int choose_tile(const GemmBatch& b) {
   if (g_tile_override != TILE_AUTO) return g_tile_override;
   int kmin = b.p[0].K;
   for (int i = 1; i < b.n_probs; ++i) kmin = b.p[i].K < kmin ? b.p[i].K : kmin;
-  if (kmin >= 4096 && tile_count(b, 256, 256) >= 128) return TILE_256x256_W8_S2;
+  if (kmin >= 4096) {
+    if (tile_count(b, 256, 256) >= 512) return TILE_256x256_W8_S2;
+    if (tile_count(b, 128, 192) >= 256) return TILE_128x192_W4_S2;
+  }
   return TILE_128x128_W4_S2;
 }
 
@@ -498,6 +504,7 @@ static hipError_t run_bf16(GemmBatch& batch, hipStream_t stream) {
     case TILE_128x128_W4_S4: return run_mfma<128, 128, 2, 2, 4, AT, BT, EPI>(batch, stream);
     case TILE_256x256_W8_S2: return run_mfma<256, 256, 2, 4, 2, AT, BT, EPI>(batch, stream);
     case TILE_256x128_W8_S3: return run_mfma<256, 128, 4, 2, 3, AT, BT, EPI>(batch, stream);
+    case TILE_128x192_W4_S2: return run_mfma<128, 192, 2, 2, 2, AT, BT, EPI>(batch, stream);
     default: return run_mfma<128, 128, 2, 2, 2, AT, BT, EPI>(batch, stream);
   }
 }

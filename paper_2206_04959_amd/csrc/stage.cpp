@@ -24,7 +24,7 @@
 #include <new>
 #include <vector>
 
-#include "../../include/merak_stage.h"
+#include "merak_stage.h"
 #include "kernels.h"
 
 using namespace merak;

@@ -30,7 +30,7 @@ ROOT = os.path.dirname(PKG)
 OUT = os.path.join(ROOT, "profiles", "gemm_dw_traffic.json")
 GEMM_SOURCE = os.path.join(PKG, "csrc", "gemm.hip")
 COPY_BYTES = 512 * 2**20  # bytes read (and written) by the reference copy
-DW_KERNEL = "true, true, 5>"  # template tail of the grouped dW GEMM instantiation (a_t, b_t, fp32 out)
+DW_KERNEL = "true, true, 5>"  # template tail of the grouped dW GEMM instantiations (a_t, b_t, fp32 out)
 COPY_KERNEL = "elementwise"   # torch's elementwise kernels (the reference copy is the last one run)
 
 
