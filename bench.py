@@ -45,7 +45,7 @@ def describe(s: synth.StageShape) -> str:
 
 
 def dw_traffic_bytes():
-    """HBM bytes per launch of the grouped weight-gradient GEMM, from the committed
+    """HBM bytes per launch of the grouped FC1/FC2 weight-gradient GEMM, from the committed
     rocprofv3 counter summary, or None if absent or taken on another kernel source."""
     try:
         with open(TRAFFIC_FILE) as f:
@@ -154,7 +154,7 @@ def main() -> int:
     exe = flops.executed_flops(shape)
     mdl = flops.model_flops(shape)
     value = exe / (ms_per_step * 1e-3) / 1e12
-    dw_per_launch = flops.dw_gemm_flops(shape)
+    dw_per_launch = flops.dw_ffn_flops(shape)
     dw_avg_ms = dw_ms / max(dw_launches, 1)
     achieved = dw_per_launch / (dw_avg_ms * 1e-3) / 1e12
     traffic = dw_traffic_bytes()
@@ -178,7 +178,8 @@ def main() -> int:
         "model_tflop_per_step": round(mdl / 1e12, 4),
         "model_tflops": round(mdl / (ms_per_step * 1e-3) / 1e12, 2),
         "roofline": {
-            "kernel": "grouped weight-gradient GEMM (gemm_mfma_kernel, a_t=b_t=1, fp32 out), one launch per block",
+            "kernel": "grouped weight-gradient GEMM of FC1 and FC2 (gemm_mfma_kernel, a_t=b_t=1, fp32 out), "
+                      "one launch per block",
             "bound": "mfma",
             "achieved": round(achieved, 2),
             "peak": PEAK_BF16_TFLOPS,

@@ -184,13 +184,14 @@ typedef enum {
   MERAK_KC_NONE = 0,
   MERAK_KC_GEMM_FWD = 1,   /* QKV, projection, FC1, FC2 GEMMs (forward and recompute)    */
   MERAK_KC_GEMM_DX = 2,    /* input-gradient GEMMs of the backward pass                  */
-  MERAK_KC_GEMM_DW = 3,    /* grouped weight-gradient GEMM, one launch per block         */
+  MERAK_KC_GEMM_DW = 3,    /* weight-gradient GEMMs of FC1 and FC2, one launch per block */
   MERAK_KC_ATTN_FWD = 4,   /* attention forward                                          */
   MERAK_KC_ATTN_BWD = 5,   /* attention backward (delta, dK/dV and dQ kernels)           */
   MERAK_KC_LN_FWD = 6,     /* LayerNorm forward                                          */
   MERAK_KC_LN_BWD = 7,     /* LayerNorm backward (input gradient)                        */
   MERAK_KC_REDUCE = 8,     /* bias / LayerNorm parameter gradient reductions             */
-  MERAK_KC_COUNT = 9
+  MERAK_KC_GEMM_DW_ATTN = 9, /* weight-gradient GEMMs of QKV and projection, one per block */
+  MERAK_KC_COUNT = 10
 } merak_kernel_class;
 
 /* Measurement aid: from now on, bracket every launch of `kernel_class` made by
@@ -234,9 +235,9 @@ int merak_gemm(int dtype, int a_trans, int b_trans, int epilogue, int M, int N, 
                const void* resid, void* aux, int accumulate, void* stream);
 
 /* Tile-shape override of the bf16 GEMM kernel, for tests and tuning:
- * 0 restores the built-in choice, 1..9 force one shape (256x256/4 waves/2
+ * 0 restores the built-in choice, 1..10 force one shape (256x256/4 waves/2
  * stages, 256x128/4/3, 128x256/4/3, 128x128/4/2, 128x128/4/3, 128x128/4/4,
- * 256x256/8/2, 256x128/8/3, 128x192/4/2).  Process-wide; returns the previous value, or -1
+ * 256x256/8/2, 256x128/8/3, 128x192/4/2, 256x192/8/2).  Process-wide; returns the previous value, or -1
  * for an out-of-range cfg (nothing changed).  Host-only, not thread-safe. */
 int merak_gemm_tile_override(int cfg);
 

@@ -24,7 +24,7 @@ STATUS = {0: "MERAK_OK", -1: "MERAK_ERR_INVALID_ARG", -2: "MERAK_ERR_SHAPE", -3:
 
 EPI_STORE, EPI_BIAS, EPI_BIAS_GELU, EPI_BIAS_RESID, EPI_GELU_BWD, EPI_F32 = range(6)
 (KC_NONE, KC_GEMM_FWD, KC_GEMM_DX, KC_GEMM_DW, KC_ATTN_FWD, KC_ATTN_BWD, KC_LN_FWD, KC_LN_BWD,
- KC_REDUCE) = range(9)
+ KC_REDUCE, KC_GEMM_DW_ATTN) = range(10)
 
 
 class MerakError(RuntimeError):
@@ -239,7 +239,7 @@ def gemm(a, b, c, M, N, K, a_trans=False, b_trans=False, epilogue=EPI_STORE, bia
 
 
 def gemm_tile_override(cfg: int) -> int:
-    """Force a bf16 GEMM tile shape (1..9) or restore the built-in choice (0);
+    """Force a bf16 GEMM tile shape (1..10) or restore the built-in choice (0);
     returns the previous setting."""
     prev = int(lib().merak_gemm_tile_override(int(cfg)))
     if prev < 0:

@@ -321,9 +321,12 @@ int block_forward(merak_stage* S, const void* params, int l, int j, char* A, con
   return MERAK_OK;
 }
 
-// Input-gradient chain of block l for sub-micro-batch j.
-int block_backward_chain(merak_stage* S, const void* params, int l, int j, const char* A, const char* x,
-                         const char* dy, char* dx, char* B, char* d_ln1, char* d_ln2, hipStream_t st) {
+// Step k (0..6) of the input-gradient chain of block l for sub-micro-batch j:
+//   0 FC2 dX (+GeLU')  1 FC1 dX  2 LN2 bwd  3 proj dX  4 attention bwd
+//   5 QKV dX  6 LN1 bwd.
+constexpr int kChainSteps = 7;
+int block_backward_step(merak_stage* S, const void* params, int l, int j, int k, const char* A, const char* x,
+                        const char* dy, char* dx, char* B, char* d_ln1, char* d_ln2, hipStream_t st) {
   const Dims& D = S->D;
   const ActLayout& L = S->W.act;
   const BwdLayout& Bl = S->W.bwd;
@@ -331,68 +334,89 @@ int block_backward_chain(merak_stage* S, const void* params, int l, int j, const
   const size_t r0 = (size_t)j * D.Ms;
   const size_t e = D.esz;
   const int M = D.Ms;
-  // FC2 backward: dg = dy W2; du = dg * gelu'(u)
-  GemmProblem p = gp(M, D.fl, D.h, dy + r0 * D.h * e, D.h, P(params, S, l, P_W2), D.fl, B + Bl.du + r0 * D.fl * e,
-                     D.fl, nullptr, nullptr, (void*)(A + L.u + r0 * D.fl * e));
-  LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(dt, false, true, EPI_GELU_BWD, &p, 1, st));
-  // FC1 backward: d_ln2 partial = du W1 (hand-off)
-  p = gp(M, D.h, D.fl, B + Bl.du + r0 * D.fl * e, D.fl, P(params, S, l, P_W1), D.h, d_ln2 + r0 * D.h * e, D.h);
-  LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(dt, false, true, EPI_STORE, &p, 1, st));
-  // LN2 backward + residual gradient: dx1 = dy + LN2'(d_ln2)
-  LAUNCH(MERAK_KC_LN_BWD, st, launch_layernorm_bwd(dt, M, D.h, d_ln2 + r0 * D.h * e, A + L.x1 + r0 * D.h * e,
-                               (const float*)(A + L.mu2) + r0, (const float*)(A + L.rs2) + r0,
-                               P(params, S, l, P_LN2G), dy + r0 * D.h * e, B + Bl.dx1 + r0 * D.h * e, st));
-  // projection backward: dO = dx1 W_o
-  p = gp(M, D.hl, D.h, B + Bl.dx1 + r0 * D.h * e, D.h, P(params, S, l, P_WO), D.hl, B + Bl.dO + r0 * D.hl * e, D.hl);
-  LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(dt, false, true, EPI_STORE, &p, 1, st));
-  // attention backward -> dqkv
-  const size_t lse_off = (size_t)j * D.bs * D.al * D.s;
-  LAUNCH(MERAK_KC_ATTN_BWD, st, launch_attention_bwd(dt, D.bs, D.s, D.al, D.d, A + L.qkv + r0 * 3 * D.hl * e, A + L.o + r0 * D.hl * e,
-                               (const float*)(A + L.lse) + lse_off, B + Bl.dO + r0 * D.hl * e,
-                               B + Bl.dqkv + r0 * 3 * D.hl * e, (float*)(B + Bl.delta) + lse_off, st));
-  // QKV backward: d_ln1 partial = dqkv W_qkv (hand-off)
-  p = gp(M, D.h, 3 * D.hl, B + Bl.dqkv + r0 * 3 * D.hl * e, 3 * D.hl, P(params, S, l, P_WQKV), D.h,
-         d_ln1 + r0 * D.h * e, D.h);
-  LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(dt, false, true, EPI_STORE, &p, 1, st));
-  // LN1 backward + residual gradient: dx = dx1 + LN1'(d_ln1)
-  LAUNCH(MERAK_KC_LN_BWD, st, launch_layernorm_bwd(dt, M, D.h, d_ln1 + r0 * D.h * e, x + r0 * D.h * e, (const float*)(A + L.mu1) + r0,
-                               (const float*)(A + L.rs1) + r0, P(params, S, l, P_LN1G), B + Bl.dx1 + r0 * D.h * e,
-                               dx + r0 * D.h * e, st));
+  GemmProblem p;
+  switch (k) {
+    case 0:  // FC2 backward: dg = dy W2; du = dg * gelu'(u)
+      p = gp(M, D.fl, D.h, dy + r0 * D.h * e, D.h, P(params, S, l, P_W2), D.fl, B + Bl.du + r0 * D.fl * e, D.fl,
+             nullptr, nullptr, (void*)(A + L.u + r0 * D.fl * e));
+      LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(dt, false, true, EPI_GELU_BWD, &p, 1, st));
+      break;
+    case 1:  // FC1 backward: d_ln2 partial = du W1 (hand-off)
+      p = gp(M, D.h, D.fl, B + Bl.du + r0 * D.fl * e, D.fl, P(params, S, l, P_W1), D.h, d_ln2 + r0 * D.h * e, D.h);
+      LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(dt, false, true, EPI_STORE, &p, 1, st));
+      break;
+    case 2:  // LN2 backward + residual gradient: dx1 = dy + LN2'(d_ln2)
+      LAUNCH(MERAK_KC_LN_BWD, st, launch_layernorm_bwd(dt, M, D.h, d_ln2 + r0 * D.h * e, A + L.x1 + r0 * D.h * e,
+                                 (const float*)(A + L.mu2) + r0, (const float*)(A + L.rs2) + r0,
+                                 P(params, S, l, P_LN2G), dy + r0 * D.h * e, B + Bl.dx1 + r0 * D.h * e, st));
+      break;
+    case 3:  // projection backward: dO = dx1 W_o
+      p = gp(M, D.hl, D.h, B + Bl.dx1 + r0 * D.h * e, D.h, P(params, S, l, P_WO), D.hl, B + Bl.dO + r0 * D.hl * e,
+             D.hl);
+      LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(dt, false, true, EPI_STORE, &p, 1, st));
+      break;
+    case 4: {  // attention backward -> dqkv
+      const size_t lse_off = (size_t)j * D.bs * D.al * D.s;
+      LAUNCH(MERAK_KC_ATTN_BWD, st, launch_attention_bwd(dt, D.bs, D.s, D.al, D.d, A + L.qkv + r0 * 3 * D.hl * e,
+                                   A + L.o + r0 * D.hl * e, (const float*)(A + L.lse) + lse_off,
+                                   B + Bl.dO + r0 * D.hl * e, B + Bl.dqkv + r0 * 3 * D.hl * e,
+                                   (float*)(B + Bl.delta) + lse_off, st));
+      break;
+    }
+    case 5:  // QKV backward: d_ln1 partial = dqkv W_qkv (hand-off)
+      p = gp(M, D.h, 3 * D.hl, B + Bl.dqkv + r0 * 3 * D.hl * e, 3 * D.hl, P(params, S, l, P_WQKV), D.h,
+             d_ln1 + r0 * D.h * e, D.h);
+      LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(dt, false, true, EPI_STORE, &p, 1, st));
+      break;
+    default:  // LN1 backward + residual gradient: dx = dx1 + LN1'(d_ln1)
+      LAUNCH(MERAK_KC_LN_BWD, st, launch_layernorm_bwd(dt, M, D.h, d_ln1 + r0 * D.h * e, x + r0 * D.h * e,
+                                 (const float*)(A + L.mu1) + r0, (const float*)(A + L.rs1) + r0,
+                                 P(params, S, l, P_LN1G), B + Bl.dx1 + r0 * D.h * e, dx + r0 * D.h * e, st));
+      break;
+  }
   return MERAK_OK;
 }
 
-// Weight, bias and LayerNorm gradients of block l over the whole micro-batch.
-int block_param_grads(merak_stage* S, int l, const char* A, const char* x, const char* dy, const char* B,
+// Weight, bias and LayerNorm gradients of block l over the whole micro-batch,
+// in two groups: group 0 (W2, b2, W1, b1) needs only dy and du, i.e. the FC2
+// backward of every sub-micro-batch; group 1 (W_o, b_o, W_qkv, b_qkv and both
+// LayerNorms) needs the rest of the chain.
+int block_param_grads(merak_stage* S, int l, int group, const char* A, const char* x, const char* dy, const char* B,
                       const char* d_ln1, const char* d_ln2, float* grads, int acc, hipStream_t st) {
   const Dims& D = S->D;
   const ActLayout& L = S->W.act;
   const BwdLayout& Bl = S->W.bwd;
   const int dt = D.dtype;
   const int T = D.T;
+  const int G = (int)reduce_groups(T);
   float* g = grads + S->p_stride * l;
-  // dW = dY^T X for the four linear layers, one grouped launch.
-  GemmProblem p[4];
+  float* pb;
+  if (group == 0) {
+    // dW = dY^T X for FC2 and FC1, one grouped launch
+    GemmProblem p[2];
+    p[0] = gp(D.h, D.fl, T, dy, D.h, A + L.g, D.fl, g + S->p_off[P_W2], D.fl, nullptr, nullptr, nullptr, acc);
+    p[1] = gp(D.fl, D.h, T, B + Bl.du, D.fl, A + L.ln2, D.h, g + S->p_off[P_W1], D.h, nullptr, nullptr, nullptr, acc);
+    LAUNCH(MERAK_KC_GEMM_DW, st, launch_gemm(dt, true, true, EPI_F32, p, 2, st));
+    // bias gradients: token sums of the layer output gradients
+    pb = (float*)(B + Bl.p_b2);
+    LAUNCH(MERAK_KC_REDUCE, st, launch_column_partials(dt, T, D.h, dy, pb, st));
+    LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials(G, D.h, pb, g + S->p_off[P_B2], acc, st));
+    pb = (float*)(B + Bl.p_b1);
+    LAUNCH(MERAK_KC_REDUCE, st, launch_column_partials(dt, T, D.fl, B + Bl.du, pb, st));
+    LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials(G, D.fl, pb, g + S->p_off[P_B1], acc, st));
+    return MERAK_OK;
+  }
+  GemmProblem p[2];
   p[0] = gp(3 * D.hl, D.h, T, B + Bl.dqkv, 3 * D.hl, A + L.ln1, D.h, g + S->p_off[P_WQKV], D.h, nullptr, nullptr,
             nullptr, acc);
   p[1] = gp(D.h, D.hl, T, B + Bl.dx1, D.h, A + L.o, D.hl, g + S->p_off[P_WO], D.hl, nullptr, nullptr, nullptr, acc);
-  p[2] = gp(D.fl, D.h, T, B + Bl.du, D.fl, A + L.ln2, D.h, g + S->p_off[P_W1], D.h, nullptr, nullptr, nullptr, acc);
-  p[3] = gp(D.h, D.fl, T, dy, D.h, A + L.g, D.fl, g + S->p_off[P_W2], D.fl, nullptr, nullptr, nullptr, acc);
-  LAUNCH(MERAK_KC_GEMM_DW, st, launch_gemm(dt, true, true, EPI_F32, p, 4, st));
-  // bias gradients: token sums of the layer output gradients
-  const int G = (int)reduce_groups(T);
-  float* pb;
+  LAUNCH(MERAK_KC_GEMM_DW_ATTN, st, launch_gemm(dt, true, true, EPI_F32, p, 2, st));
   pb = (float*)(B + Bl.p_bqkv);
   LAUNCH(MERAK_KC_REDUCE, st, launch_column_partials(dt, T, 3 * D.hl, B + Bl.dqkv, pb, st));
   LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials(G, 3 * D.hl, pb, g + S->p_off[P_BQKV], acc, st));
   pb = (float*)(B + Bl.p_bo);
   LAUNCH(MERAK_KC_REDUCE, st, launch_column_partials(dt, T, D.h, B + Bl.dx1, pb, st));
   LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials(G, D.h, pb, g + S->p_off[P_BO], acc, st));
-  pb = (float*)(B + Bl.p_b1);
-  LAUNCH(MERAK_KC_REDUCE, st, launch_column_partials(dt, T, D.fl, B + Bl.du, pb, st));
-  LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials(G, D.fl, pb, g + S->p_off[P_B1], acc, st));
-  pb = (float*)(B + Bl.p_b2);
-  LAUNCH(MERAK_KC_REDUCE, st, launch_column_partials(dt, T, D.h, dy, pb, st));
-  LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials(G, D.h, pb, g + S->p_off[P_B2], acc, st));
   // LayerNorm parameters
   float* pg = (float*)(B + Bl.p_g2);
   float* pbe = (float*)(B + Bl.p_be2);
@@ -402,8 +426,8 @@ int block_param_grads(merak_stage* S, int l, const char* A, const char* x, const
   LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials(G, D.h, pbe, g + S->p_off[P_LN2B], acc, st));
   pg = (float*)(B + Bl.p_g1);
   pbe = (float*)(B + Bl.p_be1);
-  LAUNCH(MERAK_KC_REDUCE, st, launch_layernorm_param_partials(dt, T, D.h, d_ln1, x, (const float*)(A + L.mu1), (const float*)(A + L.rs1),
-                                          pg, pbe, st));
+  LAUNCH(MERAK_KC_REDUCE, st, launch_layernorm_param_partials(dt, T, D.h, d_ln1, x, (const float*)(A + L.mu1),
+                                          (const float*)(A + L.rs1), pg, pbe, st));
   LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials(G, D.h, pg, g + S->p_off[P_LN1G], acc, st));
   LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials(G, D.h, pbe, g + S->p_off[P_LN1B], acc, st));
   return MERAK_OK;
@@ -659,13 +683,20 @@ int merak_stage_bwd(merak_stage_t S, const void* params, const void* dy, void* d
       HIP_TRY(hipStreamWaitEvent(s0, S->ev_dw[par], 0));
       HIP_TRY(hipStreamWaitEvent(s1, S->ev_dw[par], 0));
     }
-    for (int j = 0; j < D.n; ++j)
-      TRY(block_backward_chain(S, params, l, j, A, xin, dyl, dxl, B, d1, d2, (j & 1) ? s1 : s0));
-    HIP_TRY(hipEventRecord(S->ev_j0, s0));
-    HIP_TRY(hipEventRecord(S->ev_j1, s1));
-    HIP_TRY(hipStreamWaitEvent(S->aux, S->ev_j0, 0));
-    HIP_TRY(hipStreamWaitEvent(S->aux, S->ev_j1, 0));
-    TRY(block_param_grads(S, l, A, xin, dyl, B, d1, d2, grads, accumulate, S->aux));
+    // Chains issued step by step over the sub-micro-batches (sub-micro-batch j
+    // on stream j mod 2), so that the FFN weight gradients can start on the
+    // internal stream once every FC2 backward is done.
+    for (int k = 0; k < kChainSteps; ++k) {
+      for (int j = 0; j < D.n; ++j)
+        TRY(block_backward_step(S, params, l, j, k, A, xin, dyl, dxl, B, d1, d2, (j & 1) ? s1 : s0));
+      if (k == 0 || k == kChainSteps - 1) {
+        HIP_TRY(hipEventRecord(S->ev_j0, s0));
+        HIP_TRY(hipEventRecord(S->ev_j1, s1));
+        HIP_TRY(hipStreamWaitEvent(S->aux, S->ev_j0, 0));
+        HIP_TRY(hipStreamWaitEvent(S->aux, S->ev_j1, 0));
+        TRY(block_param_grads(S, l, k == 0 ? 0 : 1, A, xin, dyl, B, d1, d2, grads, accumulate, S->aux));
+      }
+    }
     HIP_TRY(hipEventRecord(S->ev_dw[par], S->aux));
   }
   HIP_TRY(hipEventRecord(S->ev_aux, S->aux));

@@ -35,6 +35,12 @@ def model_flops(s: StageShape) -> float:
 
 
 def dw_gemm_flops(s: StageShape) -> float:
-    """The grouped weight-gradient GEMM of one block (= the block's forward GEMM work)."""
+    """All weight-gradient GEMMs of one block (= the block's forward GEMM work)."""
     T, h, hl, fl = s.tokens, s.hidden, s.local_hidden, s.local_ffn
     return 2.0 * T * (3 * hl * h + h * hl + fl * h + h * fl)
+
+
+def dw_ffn_flops(s: StageShape) -> float:
+    """The grouped weight-gradient GEMM of FC1 and FC2 of one block (one launch)."""
+    T, h, fl = s.tokens, s.hidden, s.local_ffn
+    return 2.0 * T * (fl * h + h * fl)

@@ -1,4 +1,4 @@
-"""HBM traffic of the grouped weight-gradient GEMM, from rocprofv3 counters.
+"""HBM traffic of the grouped FC1/FC2 weight-gradient GEMM, from rocprofv3 counters.
 
 Two steps, each run from the repository root on the GPU machine:
 
@@ -10,9 +10,10 @@ Two steps, each run from the repository root on the GPU machine:
 
 `run` performs one fwd -> recompute -> bwd step of the 8.3B-shaped stage shard
 (through the C ABI) and one plain copy kernel of a known size (an elementwise multiply by 1).
-`summarize` reads both counter files, takes the counters of the grouped
-weight-gradient launches (fp32-output GEMM with both operands read transposed)
-and of the copy, scales the GEMM's readings by (known copy bytes / copy
+`summarize` reads both counter files, takes the counters of the grouped FC1/FC2
+weight-gradient launches (the fp32-output GEMM with both operands read
+transposed and the largest grid: the other weight-gradient launch of a block,
+QKV and projection, has fewer tiles) and of the copy, scales the GEMM's readings by (known copy bytes / copy
 reading), and writes profiles/gemm_dw_traffic.json, keyed by the SHA-256 of the
 GEMM source so that a later kernel change invalidates it.
 """
@@ -66,7 +67,7 @@ def run() -> None:
 
 
 def _dispatch_values(d: str, counter: str):
-    """{dispatch id: (kernel name, summed counter value)} from one rocprofv3 output directory."""
+    """{dispatch id: (kernel name, grid size, summed counter value)} from one rocprofv3 output directory."""
     files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
     if not files:
         raise FileNotFoundError(f"no counter_collection.csv under {d}")
@@ -75,16 +76,20 @@ def _dispatch_values(d: str, counter: str):
         for r in csv.DictReader(open(f)):
             if r["Counter_Name"] != counter:
                 continue
-            k = (f, r["Dispatch_Id"])
-            name, v = out.get(k, (r["Kernel_Name"], 0.0))
-            out[k] = (name, v + float(r["Counter_Value"]))
-    return out
+            k = (f, int(r["Dispatch_Id"]))
+            name, grid, v = out.get(k, (r["Kernel_Name"], int(r["Grid_Size"]), 0.0))
+            out[k] = (name, grid, v + float(r["Counter_Value"]))
+    return dict(sorted(out.items()))
 
 
-def _pick(vals, needle: str, last_only: bool = False):
-    sel = [v for (name, v) in vals.values() if needle in name]
+def _pick(vals, needle: str, last_only: bool = False, largest_grid: bool = False):
+    sel = [(grid, v) for (name, grid, v) in vals.values() if needle in name]
     if not sel:
         raise ValueError(f"no dispatch of a kernel containing {needle!r}")
+    if largest_grid:
+        g = max(grid for grid, _ in sel)
+        sel = [(grid, v) for grid, v in sel if grid == g]
+    sel = [v for _, v in sel]
     return sel[-1:] if last_only else sel
 
 
@@ -95,10 +100,10 @@ def summarize(dir_fetch: str, dir_write: str) -> dict:
     f_copy = _pick(fetch, COPY_KERNEL, last_only=True)[0] * 1024.0
     w_copy = _pick(write, COPY_KERNEL, last_only=True)[0] * 1024.0
     f_scale, w_scale = COPY_BYTES / f_copy, COPY_BYTES / w_copy
-    f_dw = [v * 1024.0 * f_scale for v in _pick(fetch, DW_KERNEL)]
-    w_dw = [v * 1024.0 * w_scale for v in _pick(write, DW_KERNEL)]
+    f_dw = [v * 1024.0 * f_scale for v in _pick(fetch, DW_KERNEL, largest_grid=True)]
+    w_dw = [v * 1024.0 * w_scale for v in _pick(write, DW_KERNEL, largest_grid=True)]
     res = {
-        "kernel": "grouped weight-gradient GEMM of one block (gpt-8.3b-tp4 stage shard)",
+        "kernel": "grouped FC1/FC2 weight-gradient GEMM of one block (gpt-8.3b-tp4 stage shard)",
         "launches": len(f_dw),
         "fetch_bytes_per_launch": sum(f_dw) / len(f_dw),
         "write_bytes_per_launch": sum(w_dw) / len(w_dw),

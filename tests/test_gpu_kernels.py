@@ -172,7 +172,7 @@ def test_attention_fwd_bwd(dtype, d, seq, batch, heads):
     assert rel_err(g[:, :, 2], dv) < tol
 
 
-@pytest.mark.parametrize("cfg", list(range(1, 10)))
+@pytest.mark.parametrize("cfg", list(range(1, 11)))
 @pytest.mark.parametrize("a_t,b_t", [(0, 0), (0, 1), (1, 1), (1, 0)])
 def test_gemm_every_tile_shape(cfg, a_t, b_t):
     """Each tile shape of the bf16 kernel on a ragged problem (M, N not
