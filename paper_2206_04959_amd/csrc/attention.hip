@@ -58,20 +58,28 @@ struct AttnTile {
   static constexpr int BYTES = 64 * LD * 2;  // = CPR * 1024
 };
 
-// One wave copies rows 0..63 of `src` (row stride gs elements) into the padded
-// tile at `lds` with loads that write LDS directly (lane i of instruction q
-// fills chunk 64 q + i; padding chunks re-read a data chunk).
+// One wave's plan for copying rows 0..63 of a tensor (row stride gs
+// elements) into the padded tile with loads that write LDS directly: lane i of
+// instruction q fills chunk 64 q + i (padding chunks re-read a data chunk).
+// The per-lane element offsets are computed once.
 template <int D>
-__device__ __forceinline__ void wave_tile_load(char* lds, const bf16_t* src, size_t gs, int lane) {
+struct TileLoad {
   using TT = AttnTile<D>;
+  uint32_t off[TT::CPR];
+  __device__ __forceinline__ void init(size_t gs, int lane) {
 #pragma unroll
-  for (int q = 0; q < TT::CPR; ++q) {
-    const int c = q * 64 + lane;
-    const int row = c / TT::CPR, ch = c % TT::CPR;
-    const bf16_t* g = src + (size_t)row * gs + (ch < TT::DC ? ch : 0) * 8;
-    __builtin_amdgcn_global_load_lds(g, (MERAK_LDS void*)(lds + q * 1024), 16, 0, 0);
+    for (int q = 0; q < TT::CPR; ++q) {
+      const int c = q * 64 + lane;
+      const int row = c / TT::CPR, ch = c % TT::CPR;
+      off[q] = (uint32_t)(row * gs) + (uint32_t)(ch < TT::DC ? ch : 0) * 8u;
+    }
   }
-}
+  __device__ __forceinline__ void issue(char* lds, const bf16_t* src) const {
+#pragma unroll
+    for (int q = 0; q < TT::CPR; ++q)
+      __builtin_amdgcn_global_load_lds(src + off[q], (MERAK_LDS void*)(lds + q * 1024), 16, 0, 0);
+  }
+};
 
 // 64 floats (one per lane) into LDS with a direct load.
 __device__ __forceinline__ void wave_vec_load(char* lds, const float* src, int lane) {
@@ -139,10 +147,12 @@ __global__ void __launch_bounds__(256) attn_fwd_bf16(int S, int H, const bf16_t*
 
   const int n_kb = qt + 1;  // key blocks 0..qt reach the tile's last row
   const int n_it = (n_kb + 1) / 2;
+  TileLoad<D> tl;
+  tl.init(rs, lane);
+  const bf16_t* lsrc = (wave >> 1) ? Vp : Kp;
   auto load_stage = [&](int it, int stage) {  // wave w: tile w of the stage
     const int blk = 2 * it + (wave & 1);
-    if (blk < n_kb)
-      wave_tile_load<D>(smem + (stage * 4 + wave) * TB, ((wave >> 1) ? Vp : Kp) + (size_t)blk * 64 * rs, rs, lane);
+    if (blk < n_kb) tl.issue(smem + (stage * 4 + wave) * TB, lsrc + (size_t)blk * 64 * rs);
   };
 
   f32x16_t oacc[DT];
@@ -171,31 +181,44 @@ __global__ void __launch_bounds__(256) attn_fwd_bf16(int S, int H, const bf16_t*
         s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_row<LD>(Kt, t * 32 + l32, ks * 16 + hf * 8), qf[ks],
                                                        s[t], 0, 0, 0);
     }
-    // s[t][r]: key k0 + t*32 + (r/4)*8 + 4*hf + r%4, query q
+    // s[t][r]: key k0 + t*32 + (r/4)*8 + 4*hf + r%4, query q.  Only a block
+    // that reaches past the wave's first query needs the causal mask.
     float mloc = -INFINITY;
+    if (k0 + 63 > q0) {
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+      for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = k0 + t * 32 + (r >> 2) * 8 + hf * 4 + (r & 3);
-        const float v = key > q ? -INFINITY : s[t][r] * scale_log2;
-        s[t][r] = v;
-        mloc = fmaxf(mloc, v);
-      }
+        for (int r = 0; r < 16; ++r) {
+          const int key = k0 + t * 32 + (r >> 2) * 8 + hf * 4 + (r & 3);
+          const float v = key > q ? -INFINITY : s[t][r] * scale_log2;
+          s[t][r] = v;
+          mloc = fmaxf(mloc, v);
+        }
+    } else {
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          s[t][r] *= scale_log2;
+          mloc = fmaxf(mloc, s[t][r]);
+        }
+    }
     mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
     const float mnew = fmaxf(m, mloc);
-    const float alpha = exp2f(m - mnew);
-    m = mnew;
-    l *= alpha;
+    if (__ballot(mnew > m)) {  // rescale only when some row's maximum grew
+      const float alpha = __builtin_amdgcn_exp2f(m - mnew);
+      l *= alpha;
 #pragma unroll
-    for (int t = 0; t < DT; ++t)
+      for (int t = 0; t < DT; ++t)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) oacc[t][r] *= alpha;
+        for (int r = 0; r < 16; ++r) oacc[t][r] *= alpha;
+      m = mnew;
+    }
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = exp2f(s[t][r] - mnew);
+        const float p = __builtin_amdgcn_exp2f(s[t][r] - m);
         s[t][r] = p;
         l += p;
       }
@@ -227,7 +250,7 @@ __global__ void __launch_bounds__(256) attn_fwd_bf16(int S, int H, const bf16_t*
   if (kh == 1) return;
   const float m1 = xch[0], l1 = xch[1];
   const float mt = fmaxf(m, m1);
-  const float a0 = exp2f(m - mt), a1 = exp2f(m1 - mt);
+  const float a0 = __builtin_amdgcn_exp2f(m - mt), a1 = __builtin_amdgcn_exp2f(m1 - mt);
   float lt = l * a0 + l1 * a1;
   lt += __shfl_xor(lt, 32, 64);
   const float inv = 1.0f / lt;
@@ -319,14 +342,18 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_bf16(int S, int H, const bf
 
   const int n_qb = S / 64 - kt;  // query blocks kt .. S/64-1
   const int n_it = (n_qb + 1) / 2;
+  const bool is_do = (wave >> 1) != 0;
+  const size_t lgs = is_do ? ors : rs;
+  TileLoad<D> tl;
+  tl.init(lgs, lane);
+  const bf16_t* lsrc = is_do ? dOp : Qp;
+  const float* vsrc = is_do ? del_p : lse_p;
   auto load_stage = [&](int it, int stage) {
     const int blk = kt + 2 * it + (wave & 1);
     if (2 * it + (wave & 1) < n_qb) {
-      const bool is_do = (wave >> 1) != 0;
-      wave_tile_load<D>(smem + (stage * 4 + wave) * TB, is_do ? dOp + (size_t)blk * 64 * ors : Qp + (size_t)blk * 64 * rs,
-                        is_do ? ors : rs, lane);
-      float* v = vecs + stage * 256 + (wave & 1) * 64;
-      wave_vec_load(reinterpret_cast<char*>(v + (is_do ? 128 : 0)), (is_do ? del_p : lse_p) + (size_t)blk * 64, lane);
+      tl.issue(smem + (stage * 4 + wave) * TB, lsrc + (size_t)blk * 64 * lgs);
+      float* v = vecs + stage * 256 + (wave & 1) * 64 + (is_do ? 128 : 0);
+      wave_vec_load(reinterpret_cast<char*>(v), vsrc + (size_t)blk * 64, lane);
     }
   };
 
@@ -355,12 +382,14 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_bf16(int S, int H, const bf
       }
     }
     // p[t][r]: query qs + t*32 + (r/4)*8 + 4*hf + r%4, key `key`.
+    const bool diag = qs < kw0 + 32;  // some query of the block precedes some key of the wave
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int qi = t * 32 + (r >> 2) * 8 + hf * 4 + (r & 3);
-        const float pv = (key > qs + qi) ? 0.0f : exp2f(p[t][r] * scale_log2 - lse_s[qi] * kLog2e);
+        float pv = __builtin_amdgcn_exp2f(p[t][r] * scale_log2 - lse_s[qi] * kLog2e);
+        if (diag && key > qs + qi) pv = 0.0f;
         p[t][r] = pv;
         dp[t][r] = pv * (dp[t][r] - del_s[qi]);
       }
@@ -459,10 +488,12 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_bf16(int S, int H, const bf16
 
   const int n_kb = qt + 1;
   const int n_it = (n_kb + 1) / 2;
+  TileLoad<D> tl;
+  tl.init(rs, lane);
+  const bf16_t* lsrc = (wave >> 1) ? Vp : Kp;
   auto load_stage = [&](int it, int stage) {
     const int blk = 2 * it + (wave & 1);
-    if (blk < n_kb)
-      wave_tile_load<D>(smem + (stage * 4 + wave) * TB, ((wave >> 1) ? Vp : Kp) + (size_t)blk * 64 * rs, rs, lane);
+    if (blk < n_kb) tl.issue(smem + (stage * 4 + wave) * TB, lsrc + (size_t)blk * 64 * rs);
   };
 
   load_stage(0, 0);
@@ -486,12 +517,14 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_bf16(int S, int H, const bf16
                                                         dp[t], 0, 0, 0);
       }
     }
+    const bool diag = k0 + 63 > q0;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int kk = k0 + t * 32 + (r >> 2) * 8 + hf * 4 + (r & 3);
-        const float pv = kk > q ? 0.0f : exp2f(p[t][r] * scale_log2 - lse2);
+        float pv = __builtin_amdgcn_exp2f(p[t][r] * scale_log2 - lse2);
+        if (diag && kk > q) pv = 0.0f;
         dp[t][r] = pv * (dp[t][r] - del);
       }
     bf16x8_t sb[4];
@@ -645,6 +678,22 @@ __global__ void __launch_bounds__(128) attn_bwd_dkdv_f32(int B, int S, int H, co
 // ---------------------------------------------------------------------------
 // Host launchers
 // ---------------------------------------------------------------------------
+// Explicit instantiations of the bf16 kernels (the host pass then always emits
+// their launch stubs).
+#define MERAK_ATTN_INST(D)                                                                                        \
+  template __global__ void attn_fwd_bf16<D>(int, int, const bf16_t* __restrict__, bf16_t* __restrict__,          \
+                                            float* __restrict__, float);                                         \
+  template __global__ void attn_bwd_dkdv_bf16<D>(int, int, const bf16_t* __restrict__, const bf16_t* __restrict__, \
+                                                 const float* __restrict__, const float* __restrict__,           \
+                                                 bf16_t* __restrict__, float, float);                            \
+  template __global__ void attn_bwd_dq_bf16<D>(int, int, const bf16_t* __restrict__, const bf16_t* __restrict__,   \
+                                               const float* __restrict__, const float* __restrict__,             \
+                                               bf16_t* __restrict__, float, float);
+MERAK_ATTN_INST(64)
+MERAK_ATTN_INST(96)
+MERAK_ATTN_INST(128)
+#undef MERAK_ATTN_INST
+
 // Allow a kernel's dynamic LDS beyond the default limit (once per instantiation).
 template <typename K>
 static hipError_t allow_lds(K kern, size_t bytes, bool& done) {
