@@ -65,6 +65,10 @@ hipError_t launch_column_partials(int dtype, int rows, int cols, const void* x, 
 hipError_t launch_reduce_partials(int groups, int cols, const float* part, float* out, int accumulate,
                                   hipStream_t stream);
 
+// dst[c, r] = src[r, c] for a [rows, cols] matrix (rows, cols multiples of 64).
+hipError_t launch_transpose(int dtype, int rows, int cols, const void* src, int ld_src, void* dst, int ld_dst,
+                            hipStream_t stream);
+
 // Causal attention on packed qkv [batch, seq, 3, heads, d].
 hipError_t launch_attention_fwd(int dtype, int batch, int seq, int heads, int d, const void* qkv, void* o,
                                 float* lse, hipStream_t stream);

@@ -305,4 +305,52 @@ hipError_t launch_reduce_partials(int groups, int cols, const float* part, float
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Transpose dst[c, r] = src[r, c] of a [rows, cols] matrix (rows, cols
+// multiples of 64; leading dimensions in elements).  One 64 x 64 tile per
+// workgroup through LDS: rows are read and written as contiguous 16-byte
+// (bf16) or 16-byte x 2 (fp32) chunks.
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ void __launch_bounds__(256) transpose_kernel(int rows, int cols, const T* __restrict__ src, int lds_,
+                                                        T* __restrict__ dst, int ldd) {
+  __shared__ T tile[64][64 + 8 / sizeof(T) * 2];
+  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+  const int tid = threadIdx.x;
+  // 64 rows x 8 chunks of 8 elements
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int idx = tid + i * 256;
+    const int r = idx >> 3, ch = idx & 7;
+    float v[8];
+    load8(src + (size_t)(r0 + r) * lds_ + c0 + ch * 8, v);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) tile[r][ch * 8 + e] = Elem<T>::from_f(v[e]);
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int idx = tid + i * 256;
+    const int c = idx >> 3, ch = idx & 7;  // output row c (= input column), 8 input rows
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = Elem<T>::to_f(tile[ch * 8 + e][c]);
+    store8(dst + (size_t)(c0 + c) * ldd + r0 + ch * 8, v);
+  }
+}
+
+hipError_t launch_transpose(int dtype, int rows, int cols, const void* src, int ld_src, void* dst, int ld_dst,
+                            hipStream_t stream) {
+  if (rows <= 0 || cols <= 0) return hipSuccess;
+  if (rows % 64 || cols % 64) return hipErrorInvalidValue;
+  dim3 grid(cols / 64, rows / 64);
+  if (dtype == DT_BF16)
+    hipLaunchKernelGGL((transpose_kernel<bf16_t>), grid, dim3(256), 0, stream, rows, cols, (const bf16_t*)src, ld_src,
+                       (bf16_t*)dst, ld_dst);
+  else
+    hipLaunchKernelGGL((transpose_kernel<float>), grid, dim3(256), 0, stream, rows, cols, (const float*)src, ld_src,
+                       (float*)dst, ld_dst);
+  return hipGetLastError();
+}
+
 }  // namespace merak

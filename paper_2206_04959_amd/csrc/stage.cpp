@@ -164,6 +164,9 @@ struct WsLayout {
   size_t chain;       // 3 input-gradient buffers
   size_t par[2];      // backward scratch per parity
   size_t rc_y;        // recompute's (unused) block output
+  size_t wt;          // transposed weights of every block (backward input gradients)
+  size_t wt_off[4];   // per block: W_qkv^T [h][3h/t], W_o^T [h/t][h], W1^T [h][f/t], W2^T [f/t][h] (bytes)
+  size_t wt_stride;   // bytes per block
   size_t total;
   size_t recompute_total;
   int keep_slot[kMaxBlocks];  // index among kept blocks, or -1
@@ -190,6 +193,16 @@ WsLayout ws_layout(const Dims& D) {
   W.par[0] = o; o += W.bwd.size;
   W.par[1] = o; o += W.bwd.size;
   W.rc_y = o; o += (W.n_rc > 0 ? th : 0);
+  {
+    const size_t sizes[4] = {(size_t)3 * D.hl * D.h, (size_t)D.h * D.hl, (size_t)D.fl * D.h, (size_t)D.h * D.fl};
+    size_t b = 0;
+    for (int i = 0; i < 4; ++i) {
+      W.wt_off[i] = b;
+      b = align_up(b + sizes[i] * D.esz, 256);
+    }
+    W.wt_stride = b;
+  }
+  W.wt = o; o += (size_t)D.L * W.wt_stride;
   W.total = o;
   W.recompute_total = (size_t)W.n_rc * W.act.size;
   return W;
@@ -212,6 +225,7 @@ struct merak_stage {
   char* rc;
   hipStream_t aux;
   hipEvent_t ev_fork, ev_s1, ev_j0, ev_j1, ev_aux, ev_dw[2];
+  hipEvent_t ev_wt[kMaxBlocks];  // transposed weights of block l ready
   int state;  // 0 idle, 1 forward pending, 2 recomputed
   const void* x0;
   // optional per-launch event timing of one kernel class
@@ -273,6 +287,24 @@ int timed(merak_stage* S, int cls, hipStream_t st, F&& launch) {
 
 inline const char* P(const void* params, const merak_stage* S, int l, int which) {
   return (const char*)params + (S->p_stride * l + S->p_off[which]) * S->D.esz;
+}
+
+// Transposed weight i of block l (0 W_qkv^T, 1 W_o^T, 2 W1^T, 3 W2^T): the
+// weight stored [in][out], so the input-gradient GEMMs read both operands
+// along K.
+inline const char* WT(const merak_stage* S, int l, int i) {
+  return S->ws + S->W.wt + (size_t)l * S->W.wt_stride + S->W.wt_off[i];
+}
+
+// Fill the transposed weights of block l.
+int transpose_weights(merak_stage* S, const void* params, int l, hipStream_t st) {
+  const Dims& D = S->D;
+  struct T { int which, rows, cols, dst; };
+  const T t[4] = {{P_WQKV, 3 * D.hl, D.h, 0}, {P_WO, D.h, D.hl, 1}, {P_W1, D.fl, D.h, 2}, {P_W2, D.h, D.fl, 3}};
+  for (const T& x : t)
+    LAUNCH(MERAK_KC_TRANSPOSE, st, launch_transpose(D.dtype, x.rows, x.cols, P(params, S, l, x.which), x.cols,
+                                                    (void*)WT(S, l, x.dst), x.rows, st));
+  return MERAK_OK;
 }
 
 GemmProblem gp(int M, int N, int K, const void* a, int lda, const void* b, int ldb, void* c, int ldc,
@@ -337,13 +369,13 @@ int block_backward_step(merak_stage* S, const void* params, int l, int j, int k,
   GemmProblem p;
   switch (k) {
     case 0:  // FC2 backward: dg = dy W2; du = dg * gelu'(u)
-      p = gp(M, D.fl, D.h, dy + r0 * D.h * e, D.h, P(params, S, l, P_W2), D.fl, B + Bl.du + r0 * D.fl * e, D.fl,
-             nullptr, nullptr, (void*)(A + L.u + r0 * D.fl * e));
-      LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(dt, false, true, EPI_GELU_BWD, &p, 1, st));
+      p = gp(M, D.fl, D.h, dy + r0 * D.h * e, D.h, WT(S, l, 3), D.h, B + Bl.du + r0 * D.fl * e, D.fl, nullptr, nullptr,
+             (void*)(A + L.u + r0 * D.fl * e));
+      LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(dt, false, false, EPI_GELU_BWD, &p, 1, st));
       break;
     case 1:  // FC1 backward: d_ln2 partial = du W1 (hand-off)
-      p = gp(M, D.h, D.fl, B + Bl.du + r0 * D.fl * e, D.fl, P(params, S, l, P_W1), D.h, d_ln2 + r0 * D.h * e, D.h);
-      LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(dt, false, true, EPI_STORE, &p, 1, st));
+      p = gp(M, D.h, D.fl, B + Bl.du + r0 * D.fl * e, D.fl, WT(S, l, 2), D.fl, d_ln2 + r0 * D.h * e, D.h);
+      LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(dt, false, false, EPI_STORE, &p, 1, st));
       break;
     case 2:  // LN2 backward + residual gradient: dx1 = dy + LN2'(d_ln2)
       LAUNCH(MERAK_KC_LN_BWD, st, launch_layernorm_bwd(dt, M, D.h, d_ln2 + r0 * D.h * e, A + L.x1 + r0 * D.h * e,
@@ -351,9 +383,8 @@ int block_backward_step(merak_stage* S, const void* params, int l, int j, int k,
                                  P(params, S, l, P_LN2G), dy + r0 * D.h * e, B + Bl.dx1 + r0 * D.h * e, st));
       break;
     case 3:  // projection backward: dO = dx1 W_o
-      p = gp(M, D.hl, D.h, B + Bl.dx1 + r0 * D.h * e, D.h, P(params, S, l, P_WO), D.hl, B + Bl.dO + r0 * D.hl * e,
-             D.hl);
-      LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(dt, false, true, EPI_STORE, &p, 1, st));
+      p = gp(M, D.hl, D.h, B + Bl.dx1 + r0 * D.h * e, D.h, WT(S, l, 1), D.h, B + Bl.dO + r0 * D.hl * e, D.hl);
+      LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(dt, false, false, EPI_STORE, &p, 1, st));
       break;
     case 4: {  // attention backward -> dqkv
       const size_t lse_off = (size_t)j * D.bs * D.al * D.s;
@@ -364,9 +395,9 @@ int block_backward_step(merak_stage* S, const void* params, int l, int j, int k,
       break;
     }
     case 5:  // QKV backward: d_ln1 partial = dqkv W_qkv (hand-off)
-      p = gp(M, D.h, 3 * D.hl, B + Bl.dqkv + r0 * 3 * D.hl * e, 3 * D.hl, P(params, S, l, P_WQKV), D.h,
-             d_ln1 + r0 * D.h * e, D.h);
-      LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(dt, false, true, EPI_STORE, &p, 1, st));
+      p = gp(M, D.h, 3 * D.hl, B + Bl.dqkv + r0 * 3 * D.hl * e, 3 * D.hl, WT(S, l, 0), 3 * D.hl, d_ln1 + r0 * D.h * e,
+             D.h);
+      LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(dt, false, false, EPI_STORE, &p, 1, st));
       break;
     default:  // LN1 backward + residual gradient: dx = dx1 + LN1'(d_ln1)
       LAUNCH(MERAK_KC_LN_BWD, st, launch_layernorm_bwd(dt, M, D.h, d_ln1 + r0 * D.h * e, x + r0 * D.h * e,
@@ -538,8 +569,14 @@ int merak_stage_create(const merak_stage_config* cfg, void* workspace, size_t wo
     e = hipEventCreateWithFlags(ev, hipEventDisableTiming);
     if (e == hipSuccess) ++made;
   }
+  int made_wt = 0;
+  for (int l = 0; l < D.L && e == hipSuccess; ++l) {
+    e = hipEventCreateWithFlags(&S->ev_wt[l], hipEventDisableTiming);
+    if (e == hipSuccess) ++made_wt;
+  }
   if (e != hipSuccess) {
     for (int i = 0; i < made; ++i) (void)hipEventDestroy(*evs[i]);
+    for (int l = 0; l < made_wt; ++l) (void)hipEventDestroy(S->ev_wt[l]);
     if (have_stream) (void)hipStreamDestroy(S->aux);
     delete S;
     return MERAK_ERR_HIP;
@@ -557,6 +594,7 @@ int merak_stage_destroy(merak_stage_t S) {
   }
   hipEvent_t evs[] = {S->ev_fork, S->ev_s1, S->ev_j0, S->ev_j1, S->ev_aux, S->ev_dw[0], S->ev_dw[1]};
   for (hipEvent_t ev : evs) (void)hipEventDestroy(ev);
+  for (int l = 0; l < S->D.L; ++l) (void)hipEventDestroy(S->ev_wt[l]);
   for (hipEvent_t ev : S->t_ev) (void)hipEventDestroy(ev);
   (void)hipStreamDestroy(S->aux);
   delete S;
@@ -670,6 +708,12 @@ int merak_stage_bwd(merak_stage_t S, const void* params, const void* dy, void* d
   const size_t th_al = align_up(th, 256);
   TRY(fork(S, s0, s1));
   HIP_TRY(hipStreamWaitEvent(S->aux, S->ev_fork, 0));
+  // Transposed weights for the input-gradient GEMMs, made from this call's
+  // parameters on the internal stream, last block first.
+  for (int l = D.L - 1; l >= 0; --l) {
+    TRY(transpose_weights(S, params, l, S->aux));
+    HIP_TRY(hipEventRecord(S->ev_wt[l], S->aux));
+  }
   for (int l = D.L - 1; l >= 0; --l) {
     const int par = l & 1;
     char* A = block_acts(S, l, 1);
@@ -683,6 +727,8 @@ int merak_stage_bwd(merak_stage_t S, const void* params, const void* dy, void* d
       HIP_TRY(hipStreamWaitEvent(s0, S->ev_dw[par], 0));
       HIP_TRY(hipStreamWaitEvent(s1, S->ev_dw[par], 0));
     }
+    HIP_TRY(hipStreamWaitEvent(s0, S->ev_wt[l], 0));
+    HIP_TRY(hipStreamWaitEvent(s1, S->ev_wt[l], 0));
     // Chains issued step by step over the sub-micro-batches (sub-micro-batch j
     // on stream j mod 2), so that the FFN weight gradients can start on the
     // internal stream once every FC2 backward is done.
