@@ -207,6 +207,31 @@ int merak_stage_set_timing(merak_stage_t stage, int kernel_class);
 int merak_stage_read_timing(merak_stage_t stage, double* total_ms, int64_t* launches);
 
 /* ------------------------------------------------------------------------
+ * Stage-aware recomputation planner (paper Sec. 5.2).  Host-only, no GPU.
+ *
+ * Stage i of s (numbered from 1) keeps the activations of a share alpha_i of
+ * its blocks and recomputes the rest.  Keeping them costs (s - i) * alpha_i *
+ * M_a on top of the runtime memory M_r (stage i holds s - i micro-batches in
+ * flight); all stages are given the same memory, which fixes
+ *   alpha_i = min(1, (s - 1) alpha_1 / (s - i))   for 2 <= i < s - 1,
+ *   alpha_{s-1} = alpha_{s-2},  alpha_s = 1  (shifted critical path schedule).
+ * A stage with L blocks keeps floor(alpha_i * L) of them; the recompute mask
+ * (MERAK config field recompute_mask) has bits 0 .. L - keep - 1 set.
+ * ---------------------------------------------------------------------- */
+
+/* alpha[0..s-1] and masks[0..s-1] for s stages (1 <= s <= 4096), 0 <= alpha1
+ * <= 1, blocks_per_stage in 1..64.  MERAK_ERR_INVALID_ARG / MERAK_ERR_SHAPE on
+ * bad arguments (nothing written). */
+int merak_plan_recompute(int n_stages, double alpha1, int blocks_per_stage, double* alpha, uint64_t* masks);
+
+/* The largest alpha_1 on the grid 0, step, 2 step, ... (capped at 1) for which
+ * every stage fits: M_r + (s - i) alpha_i M_a <= capacity (the paper raises
+ * alpha_1 until an out-of-memory error; this memory model stands in for it).
+ * MERAK_ERR_UNSUPPORTED if even alpha_1 = 0 does not fit. */
+int merak_plan_alpha1(int n_stages, double mem_runtime, double mem_activation, double capacity, double step,
+                      double* alpha1);
+
+/* ------------------------------------------------------------------------
  * Per-kernel entry points (each launches one hot-path kernel on `stream`).
  * They exist so each kernel can be checked and timed on its own; the stage
  * calls above use the same kernels.  dtype is merak_dtype; pointers follow the

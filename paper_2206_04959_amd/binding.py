@@ -56,6 +56,9 @@ _SIGS = {
     "merak_stage_read_timing": ([_P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)], _I),
     "merak_gemm": ([_I, _I, _I, _I, _I, _I, _I, _P, _I, _P, _I, _P, _P, _P, _P, _I, _P], _I),
     "merak_gemm_tile_override": ([_I], _I),
+    "merak_plan_recompute": ([_I, ctypes.c_double, _I, _P, _P], _I),
+    "merak_plan_alpha1": ([_I, ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_double,
+                           ctypes.POINTER(ctypes.c_double)], _I),
     "merak_layernorm_fwd": ([_I, _I, _I, _F, _P, _P, _P, _P, _P, _P, _P], _I),
     "merak_reduce_scratch_elems": ([_I, _I], _SZ),
     "merak_layernorm_bwd": ([_I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _P, _P], _I),
@@ -236,6 +239,22 @@ def gemm(a, b, c, M, N, K, a_trans=False, b_trans=False, epilogue=EPI_STORE, bia
     _check(lib().merak_gemm(dt, int(a_trans), int(b_trans), epilogue, M, N, K, _ptr(a), lda, _ptr(b), ldb,
                             _ptr(c), _ptr(bias), _ptr(resid), _ptr(aux), int(accumulate), _stream(stream)),
            "merak_gemm")
+
+
+def plan_recompute(n_stages: int, alpha1: float, blocks_per_stage: int):
+    """Stage-aware recomputation plan: ([alpha_i], [recompute mask of stage i])."""
+    a = (ctypes.c_double * n_stages)()
+    m = (ctypes.c_uint64 * n_stages)()
+    _check(lib().merak_plan_recompute(n_stages, alpha1, blocks_per_stage, a, m), "merak_plan_recompute")
+    return list(a), list(m)
+
+
+def plan_alpha1(n_stages: int, mem_runtime: float, mem_activation: float, capacity: float, step: float) -> float:
+    """Largest feasible alpha_1 on the grid of `step` under the stage memory model."""
+    out = ctypes.c_double()
+    _check(lib().merak_plan_alpha1(n_stages, mem_runtime, mem_activation, capacity, step, ctypes.byref(out)),
+           "merak_plan_alpha1")
+    return float(out.value)
 
 
 def gemm_tile_override(cfg: int) -> int:

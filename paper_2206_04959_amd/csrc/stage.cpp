@@ -19,6 +19,7 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <cmath>
 #include <map>
 #include <mutex>
 #include <new>
@@ -749,6 +750,65 @@ int merak_stage_bwd(merak_stage_t S, const void* params, const void* dy, void* d
   TRY(join(S, s0, s1));
   HIP_TRY(hipStreamWaitEvent(s0, S->ev_aux, 0));
   S->state = ST_IDLE;
+  return MERAK_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Stage-aware recomputation planner (host only)
+// ---------------------------------------------------------------------------
+namespace {
+
+// Share of kept blocks of stage i (1-based) of s; `prev` is the share of stage
+// i - 1 (used by the penultimate stage).
+double plan_share(int s, int i, double alpha1, double prev) {
+  if (i == s) return 1.0;
+  if (i == 1) return alpha1;
+  if (i == s - 1) return prev;
+  const double a = (double)(s - 1) * alpha1 / (double)(s - i);
+  return a < 1.0 ? a : 1.0;
+}
+
+bool plan_fits(int s, double a1, double mr, double ma, double cap) {
+  double prev = 0.0;
+  for (int i = 1; i <= s; ++i) {
+    const double a = plan_share(s, i, a1, prev);
+    if (mr + (double)(s - i) * a * ma > cap) return false;
+    prev = a;
+  }
+  return true;
+}
+
+}  // namespace
+
+int merak_plan_recompute(int n_stages, double alpha1, int blocks_per_stage, double* alpha, uint64_t* masks) {
+  if (n_stages < 1 || n_stages > 4096 || !(alpha1 >= 0.0 && alpha1 <= 1.0) || !alpha || !masks)
+    return MERAK_ERR_INVALID_ARG;
+  if (blocks_per_stage < 1 || blocks_per_stage > 64) return MERAK_ERR_SHAPE;
+  double prev = 0.0;
+  for (int i = 1; i <= n_stages; ++i) {
+    const double a = plan_share(n_stages, i, alpha1, prev);
+    int keep = (int)std::floor(a * blocks_per_stage + 1e-12);
+    keep = keep < 0 ? 0 : (keep > blocks_per_stage ? blocks_per_stage : keep);
+    const int n_rc = blocks_per_stage - keep;
+    alpha[i - 1] = a;
+    masks[i - 1] = n_rc >= 64 ? ~(uint64_t)0 : (((uint64_t)1 << n_rc) - 1);
+    prev = a;
+  }
+  return MERAK_OK;
+}
+
+int merak_plan_alpha1(int n_stages, double mem_runtime, double mem_activation, double capacity, double step,
+                      double* alpha1) {
+  if (n_stages < 1 || n_stages > 4096 || !alpha1 || !(step > 0.0) || !(mem_activation >= 0.0))
+    return MERAK_ERR_INVALID_ARG;
+  if (!plan_fits(n_stages, 0.0, mem_runtime, mem_activation, capacity)) return MERAK_ERR_UNSUPPORTED;
+  double best = 0.0;
+  for (long k = 1; (double)k * step <= 1.0 + 1e-12; ++k) {
+    const double a1 = (double)k * step < 1.0 ? (double)k * step : 1.0;
+    if (!plan_fits(n_stages, a1, mem_runtime, mem_activation, capacity)) break;
+    best = a1;
+  }
+  *alpha1 = best;
   return MERAK_OK;
 }
 
