@@ -336,6 +336,30 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_mfma_kernel(GemmBatch batch
     if (kt + NS < KT) issue(cur);
     step(smem + ((kt + 1) % NS) * STAGE, 0, a0, b0, a1, b1);
   }
+  // acc[j][i][r]: output row m = m0 + wm*WTM + i*32 + lane%32,
+  // column n = n0 + wn*WTN + j*32 + (r/4)*8 + (lane/32)*4 + r%4.
+  auto out_m = [&](int i) { return m0 + wm * WTM + i * 32 + (lane & 31); };
+  auto out_n = [&](int j, int g) { return n0 + wn * WTN + j * 32 + g * 8 + (lane >> 5) * 4; };
+
+  // Epilogues that read a [M, N] operand (the residual, or the stored GeLU
+  // input u) fetch it before the last K stage, so the loads overlap its MFMAs
+  // (wave tiles of up to six 32 x 32 blocks: 48 extra registers).
+  constexpr bool PRE = (EPI == EPI_BIAS_RESID || EPI == EPI_GELU_BWD) && TM * TN <= 6;
+  u32x2_t pre[PRE ? TN : 1][PRE ? TM : 1][4];
+  if constexpr (PRE) {
+    const bf16_t* src = reinterpret_cast<const bf16_t*>(EPI == EPI_BIAS_RESID ? p.resid : p.aux);
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int m = out_m(i), n = out_n(j, g);
+          pre[j][i][g] = (m < p.M && n < p.N) ? *reinterpret_cast<const u32x2_t*>(src + (size_t)m * p.ldc + n)
+                                              : u32x2_t{0u, 0u};
+        }
+  }
+
   {
     const char* st = smem + ((KT - 1) % NS) * STAGE;
     step(st, 1, a1, b1, a0, b0);
@@ -343,21 +367,36 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_mfma_kernel(GemmBatch batch
     step(st, 3, a1, b1, a0, b0);
     mfmas(a1, b1);
   }
-
-  // acc[j][i][r]: output row m = m0 + wm*WTM + i*32 + lane%32,
-  // column n = n0 + wn*WTN + j*32 + (r/4)*8 + (lane/32)*4 + r%4.
 #pragma unroll
   for (int j = 0; j < TN; ++j)
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
-      const int m = m0 + wm * WTM + i * 32 + (lane & 31);
+      const int m = out_m(i);
       if (m >= p.M) continue;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int n = n0 + wn * WTN + j * 32 + g * 8 + (lane >> 5) * 4;
+        const int n = out_n(j, g);
         if (n < p.N) {
           float v[4] = {acc[j][i][4 * g], acc[j][i][4 * g + 1], acc[j][i][4 * g + 2], acc[j][i][4 * g + 3]};
-          epilogue4<bf16_t, EPI>(p, m, n, v);
+          if constexpr (PRE) {
+            const u32x2_t w = pre[j][i][g];
+            const float x[4] = {__uint_as_float(w[0] << 16), __uint_as_float(w[0] & 0xffff0000u),
+                                __uint_as_float(w[1] << 16), __uint_as_float(w[1] & 0xffff0000u)};
+            bf16_t* c = reinterpret_cast<bf16_t*>(p.c) + (size_t)m * p.ldc + n;
+            if constexpr (EPI == EPI_BIAS_RESID) {
+              if (p.aux) store4(reinterpret_cast<bf16_t*>(p.aux) + (size_t)m * p.ldc + n, v);
+              float b[4];
+              load4(reinterpret_cast<const bf16_t*>(p.bias) + n, b);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) v[e] = x[e] + v[e] + b[e];
+            } else {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) v[e] *= gelu_grad_f(x[e]);
+            }
+            store4(c, v);
+          } else {
+            epilogue4<bf16_t, EPI>(p, m, n, v);
+          }
         }
       }
       // one output block at a time (keeps the accumulators in place)
