@@ -232,6 +232,39 @@ int merak_plan_alpha1(int n_stages, double mem_runtime, double mem_activation, d
                       double* alpha1);
 
 /* ------------------------------------------------------------------------
+ * Pipeline schedules (paper Sec. 5.1).  Host-only, no GPU.
+ *
+ * Per stage, the order of its forward (F), recomputation (R) and backward (B)
+ * calls over m micro-batches; a stage runs them with merak_stage_fwd,
+ * merak_stage_recompute and merak_stage_bwd (one handle per micro-batch in
+ * flight).  Dependencies: F of stage i needs F of stage i-1, B needs B of
+ * stage i+1 and the stage's own R of that micro-batch; R needs nothing from
+ * other stages.
+ *   MERAK_SCHED_1F1B:  s-1-i warm-up forwards, then one forward / one backward,
+ *     the backward recomputing first (op MERAK_OP_RECOMPUTE_BWD);
+ *   MERAK_SCHED_EARLY_RECOMPUTE: the same with R split off, run as soon as the
+ *     stage is free;
+ *   MERAK_SCHED_SCP (shifted critical path): the last stage skips R; the
+ *     penultimate stage runs F0 F1 R0 F2 B0 and then R_j B_j F_{j+2}; the other
+ *     stages as in early recomputation.
+ * With costs F = R = T_m, B = 2 T_m the bubble ratios (makespan - 4 m T_m) /
+ * (4 m T_m) are (s-1)/m, 3(s-1)/(4m) and 3(s-2)/(4m) for m >= s.
+ * ---------------------------------------------------------------------- */
+typedef enum { MERAK_SCHED_1F1B = 0, MERAK_SCHED_EARLY_RECOMPUTE = 1, MERAK_SCHED_SCP = 2 } merak_schedule_kind;
+typedef enum { MERAK_OP_FWD = 0, MERAK_OP_RECOMPUTE = 1, MERAK_OP_BWD = 2, MERAK_OP_RECOMPUTE_BWD = 3 } merak_op_type;
+
+/* Op list of one stage: ops[k] = (type << 24) | micro_batch, k < *n_ops
+ * (at most 3 m).  1 <= n_stages <= 1024, 1 <= n_micro < 2^24, 0 <= stage <
+ * n_stages.  MERAK_ERR_WORKSPACE if capacity is too small (*n_ops = needed). */
+int merak_schedule_stage(int kind, int n_stages, int n_micro, int stage, int32_t* ops, int capacity, int* n_ops);
+
+/* Greedy in-order execution of all stages' op lists with the given costs
+ * (a recompute-in-backward op costs cost_rc + cost_bwd): the makespan and each
+ * stage's busy time (busy[0..n_stages-1]).  n_stages * n_micro <= 2^22. */
+int merak_schedule_simulate(int kind, int n_stages, int n_micro, double cost_fwd, double cost_rc, double cost_bwd,
+                            double* makespan, double* busy);
+
+/* ------------------------------------------------------------------------
  * Per-kernel entry points (each launches one hot-path kernel on `stream`).
  * They exist so each kernel can be checked and timed on its own; the stage
  * calls above use the same kernels.  dtype is merak_dtype; pointers follow the

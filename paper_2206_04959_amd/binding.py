@@ -57,6 +57,9 @@ _SIGS = {
     "merak_gemm": ([_I, _I, _I, _I, _I, _I, _I, _P, _I, _P, _I, _P, _P, _P, _P, _I, _P], _I),
     "merak_gemm_tile_override": ([_I], _I),
     "merak_plan_recompute": ([_I, ctypes.c_double, _I, _P, _P], _I),
+    "merak_schedule_stage": ([_I, _I, _I, _I, _P, _I, ctypes.POINTER(_I)], _I),
+    "merak_schedule_simulate": ([_I, _I, _I, ctypes.c_double, ctypes.c_double, ctypes.c_double,
+                                 ctypes.POINTER(ctypes.c_double), _P], _I),
     "merak_plan_alpha1": ([_I, ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_double,
                            ctypes.POINTER(ctypes.c_double)], _I),
     "merak_layernorm_fwd": ([_I, _I, _I, _F, _P, _P, _P, _P, _P, _P, _P], _I),
@@ -239,6 +242,28 @@ def gemm(a, b, c, M, N, K, a_trans=False, b_trans=False, epilogue=EPI_STORE, bia
     _check(lib().merak_gemm(dt, int(a_trans), int(b_trans), epilogue, M, N, K, _ptr(a), lda, _ptr(b), ldb,
                             _ptr(c), _ptr(bias), _ptr(resid), _ptr(aux), int(accumulate), _stream(stream)),
            "merak_gemm")
+
+
+SCHED_1F1B, SCHED_EARLY_RECOMPUTE, SCHED_SCP = range(3)
+OP_FWD, OP_RECOMPUTE, OP_BWD, OP_RECOMPUTE_BWD = range(4)
+
+
+def schedule_stage(kind: int, n_stages: int, n_micro: int, stage: int):
+    """Op list of one stage: [(op type, micro-batch)]."""
+    n = ctypes.c_int()
+    buf = (ctypes.c_int32 * (3 * n_micro + 4))()
+    _check(lib().merak_schedule_stage(kind, n_stages, n_micro, stage, buf, len(buf), ctypes.byref(n)),
+           "merak_schedule_stage")
+    return [(int(v) >> 24, int(v) & 0xFFFFFF) for v in buf[:n.value]]
+
+
+def schedule_simulate(kind: int, n_stages: int, n_micro: int, cost_fwd=1.0, cost_rc=1.0, cost_bwd=2.0):
+    """(makespan, [busy time per stage]) of the greedy in-order execution."""
+    mk = ctypes.c_double()
+    busy = (ctypes.c_double * n_stages)()
+    _check(lib().merak_schedule_simulate(kind, n_stages, n_micro, cost_fwd, cost_rc, cost_bwd, ctypes.byref(mk), busy),
+           "merak_schedule_simulate")
+    return float(mk.value), list(busy)
 
 
 def plan_recompute(n_stages: int, alpha1: float, blocks_per_stage: int):

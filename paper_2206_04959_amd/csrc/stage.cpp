@@ -19,6 +19,7 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <algorithm>
 #include <cmath>
 #include <map>
 #include <mutex>
@@ -809,6 +810,130 @@ int merak_plan_alpha1(int n_stages, double mem_runtime, double mem_activation, d
     best = a1;
   }
   *alpha1 = best;
+  return MERAK_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Pipeline schedules (host only)
+// ---------------------------------------------------------------------------
+namespace {
+
+inline int32_t sched_op(int type, int mb) { return (int32_t)(((uint32_t)type << 24) | (uint32_t)mb); }
+
+// Op list of one stage (see the header for the three orders).
+void build_stage_ops(int kind, int s, int m, int i, std::vector<int32_t>& ops) {
+  ops.clear();
+  if (kind == MERAK_SCHED_SCP && i == s - 1) {  // the last stage keeps its activation
+    for (int j = 0; j < m; ++j) {
+      ops.push_back(sched_op(MERAK_OP_FWD, j));
+      ops.push_back(sched_op(MERAK_OP_BWD, j));
+    }
+    return;
+  }
+  if (kind == MERAK_SCHED_SCP && i == s - 2 && m >= 2) {  // one forward brought ahead
+    ops.push_back(sched_op(MERAK_OP_FWD, 0));
+    ops.push_back(sched_op(MERAK_OP_FWD, 1));
+    ops.push_back(sched_op(MERAK_OP_RECOMPUTE, 0));
+    int nf = 2;
+    if (nf < m) ops.push_back(sched_op(MERAK_OP_FWD, nf++));
+    ops.push_back(sched_op(MERAK_OP_BWD, 0));
+    for (int j = 1; j < m; ++j) {
+      ops.push_back(sched_op(MERAK_OP_RECOMPUTE, j));
+      ops.push_back(sched_op(MERAK_OP_BWD, j));
+      if (nf < m) ops.push_back(sched_op(MERAK_OP_FWD, nf++));
+    }
+    return;
+  }
+  const int warm = std::min(s - 1 - i, m);
+  int nf = 0;
+  for (; nf < warm; ++nf) ops.push_back(sched_op(MERAK_OP_FWD, nf));
+  for (int j = 0; j < m; ++j) {
+    if (nf < m) ops.push_back(sched_op(MERAK_OP_FWD, nf++));
+    if (kind == MERAK_SCHED_1F1B) {
+      ops.push_back(sched_op(MERAK_OP_RECOMPUTE_BWD, j));
+    } else {
+      ops.push_back(sched_op(MERAK_OP_RECOMPUTE, j));
+      ops.push_back(sched_op(MERAK_OP_BWD, j));
+    }
+  }
+}
+
+int check_sched(int kind, int s, int m) {
+  if (kind < MERAK_SCHED_1F1B || kind > MERAK_SCHED_SCP) return MERAK_ERR_INVALID_ARG;
+  if (s < 1 || s > 1024 || m < 1 || m >= (1 << 24)) return MERAK_ERR_SHAPE;
+  return MERAK_OK;
+}
+
+}  // namespace
+
+int merak_schedule_stage(int kind, int n_stages, int n_micro, int stage, int32_t* ops, int capacity, int* n_ops) {
+  TRY(check_sched(kind, n_stages, n_micro));
+  if (stage < 0 || stage >= n_stages || !n_ops || capacity < 0 || (capacity > 0 && !ops)) return MERAK_ERR_INVALID_ARG;
+  std::vector<int32_t> v;
+  build_stage_ops(kind, n_stages, n_micro, stage, v);
+  *n_ops = (int)v.size();
+  if ((int)v.size() > capacity) return MERAK_ERR_WORKSPACE;
+  std::copy(v.begin(), v.end(), ops);
+  return MERAK_OK;
+}
+
+int merak_schedule_simulate(int kind, int n_stages, int n_micro, double cost_fwd, double cost_rc, double cost_bwd,
+                            double* makespan, double* busy) {
+  TRY(check_sched(kind, n_stages, n_micro));
+  const int s = n_stages, m = n_micro;
+  if ((int64_t)s * m > ((int64_t)1 << 22)) return MERAK_ERR_SHAPE;
+  if (!makespan || !busy || !(cost_fwd >= 0.0) || !(cost_rc >= 0.0) || !(cost_bwd >= 0.0)) return MERAK_ERR_INVALID_ARG;
+  std::vector<std::vector<int32_t>> plan(s);
+  for (int i = 0; i < s; ++i) build_stage_ops(kind, s, m, i, plan[i]);
+  // finish times per (stage, micro-batch); < 0 = not yet run
+  std::vector<double> fF((size_t)s * m, -1.0), fR((size_t)s * m, -1.0), fB((size_t)s * m, -1.0);
+  std::vector<char> hasR((size_t)s * m, 0);
+  for (int i = 0; i < s; ++i)
+    for (int32_t op : plan[i])
+      if ((op >> 24) == MERAK_OP_RECOMPUTE) hasR[(size_t)i * m + (op & 0xffffff)] = 1;
+  std::vector<double> free_at(s, 0.0), work(s, 0.0);
+  std::vector<size_t> pos(s, 0);
+  size_t left = 0;
+  for (auto& p : plan) left += p.size();
+  while (left) {
+    bool moved = false;
+    for (int i = 0; i < s; ++i) {
+      if (pos[i] == plan[i].size()) continue;
+      const int type = plan[i][pos[i]] >> 24, j = plan[i][pos[i]] & 0xffffff;
+      const size_t at = (size_t)i * m + j;
+      double ready = free_at[i];
+      bool ok = true;
+      if (type == MERAK_OP_FWD && i > 0) {
+        const double f = fF[(size_t)(i - 1) * m + j];
+        ok = ok && f >= 0.0;
+        ready = std::max(ready, f);
+      }
+      if (type == MERAK_OP_BWD || type == MERAK_OP_RECOMPUTE_BWD) {
+        if (i < s - 1) {
+          const double f = fB[(size_t)(i + 1) * m + j];
+          ok = ok && f >= 0.0;
+          ready = std::max(ready, f);
+        }
+        if (type == MERAK_OP_BWD && hasR[at]) {
+          ok = ok && fR[at] >= 0.0;
+          ready = std::max(ready, fR[at]);
+        }
+      }
+      if (!ok) continue;
+      const double cost = type == MERAK_OP_FWD ? cost_fwd
+                          : type == MERAK_OP_RECOMPUTE ? cost_rc
+                          : type == MERAK_OP_BWD ? cost_bwd : cost_rc + cost_bwd;
+      free_at[i] = ready + cost;
+      work[i] += cost;
+      (type == MERAK_OP_FWD ? fF : type == MERAK_OP_RECOMPUTE ? fR : fB)[at] = free_at[i];
+      ++pos[i];
+      --left;
+      moved = true;
+    }
+    if (!moved) return MERAK_ERR_ORDER;  // cannot happen for the built-in orders
+  }
+  *makespan = *std::max_element(free_at.begin(), free_at.end());
+  for (int i = 0; i < s; ++i) busy[i] = work[i];
   return MERAK_OK;
 }
 
