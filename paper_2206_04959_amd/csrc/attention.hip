@@ -111,9 +111,18 @@ __device__ __forceinline__ bf16x8_t frag_tr(const char* tile, int kb, int col0, 
 
 __device__ __forceinline__ bf16x8_t frag_kc(const bf16_t* p) { return *reinterpret_cast<const bf16x8_t*>(p); }
 
-// Dynamic LDS of the bf16 kernels: two stages of four tiles.
+// LDS stages of the bf16 kernels (each four tiles: two 64-row blocks of two
+// tensors).  One stage keeps a workgroup small enough (53 KB at d = 96) to share
+// a CU with a GEMM workgroup of the other stream; the loads of the next block
+// pair are then issued after the current pair has been used.
+#ifndef MERAK_ATTN_STAGES
+#define MERAK_ATTN_STAGES 1
+#endif
+constexpr int kAttnStages = MERAK_ATTN_STAGES;
+static_assert(kAttnStages == 1 || kAttnStages == 2, "one or two LDS stages");
+
 template <int D>
-constexpr size_t attn_lds_bytes() { return (size_t)8 * AttnTile<D>::BYTES; }
+constexpr size_t attn_lds_bytes() { return (size_t)kAttnStages * 4 * AttnTile<D>::BYTES; }
 
 // ---------------------------------------------------------------------------
 // bf16 forward.  A workgroup owns 64 query rows of one (batch, head); wave w
@@ -162,14 +171,19 @@ __global__ void __launch_bounds__(256) attn_fwd_bf16(int S, int H, const bf16_t*
     for (int r = 0; r < 16; ++r) oacc[t][r] = 0.0f;
   float m = -INFINITY, l = 0.0f;
 
-  load_stage(0, 0);
+  if (kAttnStages == 2) load_stage(0, 0);
   for (int it = 0; it < n_it; ++it) {
-    __syncthreads();  // stage it landed; stage it+1 no longer read
-    if (it + 1 < n_it) load_stage(it + 1, (it + 1) & 1);
+    const int cur = it % kAttnStages;
+    if (kAttnStages == 1) {
+      __syncthreads();  // every wave is done with the previous block pair
+      load_stage(it, 0);
+    }
+    __syncthreads();  // this block pair landed (and, with two stages, the other stage is free)
+    if (kAttnStages == 2 && it + 1 < n_it) load_stage(it + 1, (it + 1) % kAttnStages);
     const int kb = 2 * it + kh, k0 = kb * 64;
     if (kb >= n_kb || k0 > q0 + 31) continue;
-    const char* Kt = smem + ((it & 1) * 4 + kh) * TB;
-    const char* Vt = smem + ((it & 1) * 4 + 2 + kh) * TB;
+    const char* Kt = smem + (cur * 4 + kh) * TB;
+    const char* Vt = smem + (cur * 4 + 2 + kh) * TB;
 
     f32x16_t s[2];
 #pragma unroll
@@ -236,6 +250,7 @@ __global__ void __launch_bounds__(256) attn_fwd_bf16(int S, int H, const bf16_t*
 
   // Merge the two key halves of each query group (partial m, l, O^T).
   constexpr int XS = 2 + DT * 16;
+  static_assert((size_t)128 * XS * 4 <= (size_t)kAttnStages * 4 * TB, "merge buffer fits the tiles");
   float* xch = reinterpret_cast<float*>(smem) + (size_t)(qg * 64 + lane) * XS;
   __syncthreads();
   if (kh == 1) {
@@ -310,7 +325,7 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_bf16(int S, int H, const bf
   using TT = AttnTile<D>;
   constexpr int LD = TT::LD, KS = D / 16, DT = D / 32, TB = TT::BYTES;
   extern __shared__ __align__(16) char smem[];  // [stage][Q a, Q b, dO a, dO b], then lse/delta
-  float* vecs = reinterpret_cast<float*>(smem + 8 * TB);  // [stage][lse a|b (128), delta a|b (128)]
+  float* vecs = reinterpret_cast<float*>(smem + kAttnStages * 4 * TB);  // [stage][lse a|b, delta a|b]
 
   const int b = blockIdx.z, hh = blockIdx.y;
   const int kt = blockIdx.x;  // early keys see the most queries: dispatched first
@@ -357,15 +372,20 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_bf16(int S, int H, const bf
     }
   };
 
-  load_stage(0, 0);
+  if (kAttnStages == 2) load_stage(0, 0);
   for (int it = 0; it < n_it; ++it) {
+    const int cur = it % kAttnStages;
+    if (kAttnStages == 1) {
+      __syncthreads();
+      load_stage(it, 0);
+    }
     __syncthreads();
-    if (it + 1 < n_it) load_stage(it + 1, (it + 1) & 1);
+    if (kAttnStages == 2 && it + 1 < n_it) load_stage(it + 1, (it + 1) % kAttnStages);
     const int qb = kt + 2 * it + qh, qs = qb * 64;
     if (2 * it + qh >= n_qb || qs + 63 < kw0) continue;
-    const char* Qt = smem + ((it & 1) * 4 + qh) * TB;
-    const char* dOt = smem + ((it & 1) * 4 + 2 + qh) * TB;
-    const float* lse_s = vecs + (it & 1) * 256 + qh * 64;
+    const char* Qt = smem + (cur * 4 + qh) * TB;
+    const char* dOt = smem + (cur * 4 + 2 + qh) * TB;
+    const float* lse_s = vecs + cur * 256 + qh * 64;
     const float* del_s = lse_s + 128;
 
     f32x16_t p[2], dp[2];
@@ -413,6 +433,7 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_bf16(int S, int H, const bf
 
   // Add the two query halves.
   constexpr int XS = 2 * DT * 16;
+  static_assert((size_t)128 * XS * 4 <= (size_t)kAttnStages * 4 * TB, "merge buffer fits the tiles");
   float* xch = reinterpret_cast<float*>(smem) + (size_t)(kg * 64 + lane) * XS;
   __syncthreads();
   if (qh == 1) {
@@ -496,14 +517,19 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_bf16(int S, int H, const bf16
     if (blk < n_kb) tl.issue(smem + (stage * 4 + wave) * TB, lsrc + (size_t)blk * 64 * rs);
   };
 
-  load_stage(0, 0);
+  if (kAttnStages == 2) load_stage(0, 0);
   for (int it = 0; it < n_it; ++it) {
+    const int cur = it % kAttnStages;
+    if (kAttnStages == 1) {
+      __syncthreads();
+      load_stage(it, 0);
+    }
     __syncthreads();
-    if (it + 1 < n_it) load_stage(it + 1, (it + 1) & 1);
+    if (kAttnStages == 2 && it + 1 < n_it) load_stage(it + 1, (it + 1) % kAttnStages);
     const int kb = 2 * it + kh, k0 = kb * 64;
     if (kb >= n_kb || k0 > q0 + 31) continue;
-    const char* Kt = smem + ((it & 1) * 4 + kh) * TB;
-    const char* Vt = smem + ((it & 1) * 4 + 2 + kh) * TB;
+    const char* Kt = smem + (cur * 4 + kh) * TB;
+    const char* Vt = smem + (cur * 4 + 2 + kh) * TB;
     f32x16_t p[2], dp[2];
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
@@ -539,6 +565,7 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_bf16(int S, int H, const bf16
   }
 
   constexpr int XS = DT * 16;
+  static_assert((size_t)128 * XS * 4 <= (size_t)kAttnStages * 4 * TB, "merge buffer fits the tiles");
   float* xch = reinterpret_cast<float*>(smem) + (size_t)(qg * 64 + lane) * XS;
   __syncthreads();
   if (kh == 1) {
@@ -730,7 +757,7 @@ static hipError_t bwd_d(int dtype, int B, int S, int H, const void* qkv, const v
   const int rows = B * S * H;
   if (dtype == DT_BF16) {
     constexpr size_t lds_q = attn_lds_bytes<D>();
-    constexpr size_t lds_k = attn_lds_bytes<D>() + 2 * 256 * sizeof(float);
+    constexpr size_t lds_k = attn_lds_bytes<D>() + kAttnStages * 256 * sizeof(float);
     static_assert(lds_k <= 160 * 1024, "LDS budget");
     static bool ok_k = false, ok_q = false;
     hipError_t e = allow_lds(attn_bwd_dkdv_bf16<D>, lds_k, ok_k);
