@@ -94,18 +94,23 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
-// GeLU, tanh form, and its derivative.  tanh(z) = 1 - 2 / (exp(2z) + 1), which
-// saturates correctly for large |z|.
+// GeLU, tanh form, and its derivative, written with s = sigmoid(2z) =
+// 1 / (1 + exp(-2z)), z = sqrt(2/pi) (u + 0.044715 u^3): since
+// 1 + tanh(z) = 2 s and 1 - tanh(z)^2 = 4 s (1 - s),
+//   gelu(u)  = u s,
+//   gelu'(u) = s + 2 u s (1 - s) sqrt(2/pi) (1 + 3 * 0.044715 u^2).
+// One exponential and one hardware reciprocal (about 1 ulp) per element; both
+// saturate correctly for large |u| (exp -> inf gives s = 0, exp -> 0 gives 1).
 constexpr float kGeluC = 0.7978845608028654f;  // sqrt(2/pi)
 constexpr float kGeluA = 0.044715f;
-__device__ __forceinline__ float tanh_fast(float z) { return 1.0f - 2.0f / (__expf(2.0f * z) + 1.0f); }
-__device__ __forceinline__ float gelu_f(float u) {
-  float th = tanh_fast(kGeluC * (u + kGeluA * u * u * u));
-  return 0.5f * u * (1.0f + th);
+__device__ __forceinline__ float gelu_sigmoid(float u) {
+  const float z2 = 2.0f * kGeluC * (u + kGeluA * u * u * u);
+  return __builtin_amdgcn_rcpf(1.0f + __expf(-z2));
 }
+__device__ __forceinline__ float gelu_f(float u) { return u * gelu_sigmoid(u); }
 __device__ __forceinline__ float gelu_grad_f(float u) {
-  float th = tanh_fast(kGeluC * (u + kGeluA * u * u * u));
-  return 0.5f * (1.0f + th) + 0.5f * u * (1.0f - th * th) * kGeluC * (1.0f + 3.0f * kGeluA * u * u);
+  const float s = gelu_sigmoid(u);
+  return s + 2.0f * u * s * (1.0f - s) * kGeluC * (1.0f + 3.0f * kGeluA * u * u);
 }
 
 }  // namespace merak

@@ -317,41 +317,82 @@ GemmProblem gp(int M, int N, int K, const void* a, int lda, const void* b, int l
   return p;
 }
 
-// Forward of block l for sub-micro-batch j on stream st.
-int block_forward(merak_stage* S, const void* params, int l, int j, char* A, const char* x, char* y,
-                  char* part_o, char* part_f, hipStream_t st) {
+// Step k (0..6) of the forward of block l for sub-micro-batch j:
+//   0 LN1  1 QKV GEMM  2 attention  3 projection GEMM  4 LN2  5 FC1 GEMM
+//   6 FC2 GEMM.
+// GEMM steps only describe their problem (*p, *epi) for a grouped launch; the
+// other steps are launched on st.
+constexpr int kFwdSteps = 7;
+inline bool fwd_step_is_gemm(int k) { return k == 1 || k == 3 || k == 5 || k == 6; }
+int block_forward_step(merak_stage* S, const void* params, int l, int j, int k, char* A, const char* x, char* y,
+                       char* part_o, char* part_f, hipStream_t st, GemmProblem* p, int* epi) {
   const Dims& D = S->D;
   const ActLayout& L = S->W.act;
   const int dt = D.dtype;
   const size_t r0 = (size_t)j * D.Ms;
   const size_t e = D.esz;
   const int M = D.Ms;
-  // LN1
-  LAUNCH(MERAK_KC_LN_FWD, st, launch_layernorm_fwd(dt, M, D.h, D.eps, x + r0 * D.h * e, P(params, S, l, P_LN1G), P(params, S, l, P_LN1B),
-                               A + L.ln1 + r0 * D.h * e, (float*)(A + L.mu1) + r0, (float*)(A + L.rs1) + r0, st));
-  // QKV (column parallel) + bias
-  GemmProblem p = gp(M, 3 * D.hl, D.h, A + L.ln1 + r0 * D.h * e, D.h, P(params, S, l, P_WQKV), D.h,
-                     A + L.qkv + r0 * 3 * D.hl * e, 3 * D.hl, P(params, S, l, P_BQKV));
-  LAUNCH(MERAK_KC_GEMM_FWD, st, launch_gemm(dt, false, false, EPI_BIAS, &p, 1, st));
-  // causal attention on the local heads
-  LAUNCH(MERAK_KC_ATTN_FWD, st, launch_attention_fwd(dt, D.bs, D.s, D.al, D.d, A + L.qkv + r0 * 3 * D.hl * e, A + L.o + r0 * D.hl * e,
-                               (float*)(A + L.lse) + (size_t)j * D.bs * D.al * D.s, st));
-  // projection (row parallel): partial sum -> hand-off; x1 = x + partial + b_o
-  p = gp(M, D.h, D.hl, A + L.o + r0 * D.hl * e, D.hl, P(params, S, l, P_WO), D.hl, A + L.x1 + r0 * D.h * e, D.h,
-         P(params, S, l, P_BO), x + r0 * D.h * e, part_o ? part_o + r0 * D.h * e : nullptr);
-  LAUNCH(MERAK_KC_GEMM_FWD, st, launch_gemm(dt, false, false, EPI_BIAS_RESID, &p, 1, st));
-  // LN2
-  LAUNCH(MERAK_KC_LN_FWD, st, launch_layernorm_fwd(dt, M, D.h, D.eps, A + L.x1 + r0 * D.h * e, P(params, S, l, P_LN2G),
-                               P(params, S, l, P_LN2B), A + L.ln2 + r0 * D.h * e, (float*)(A + L.mu2) + r0,
-                               (float*)(A + L.rs2) + r0, st));
-  // FC1 (column parallel) + bias + GeLU; keeps the pre-activation u
-  p = gp(M, D.fl, D.h, A + L.ln2 + r0 * D.h * e, D.h, P(params, S, l, P_W1), D.h, A + L.g + r0 * D.fl * e, D.fl,
-         P(params, S, l, P_B1), nullptr, A + L.u + r0 * D.fl * e);
-  LAUNCH(MERAK_KC_GEMM_FWD, st, launch_gemm(dt, false, false, EPI_BIAS_GELU, &p, 1, st));
-  // FC2 (row parallel): partial sum -> hand-off; y = x1 + partial + b2
-  p = gp(M, D.h, D.fl, A + L.g + r0 * D.fl * e, D.fl, P(params, S, l, P_W2), D.fl, y + r0 * D.h * e, D.h,
-         P(params, S, l, P_B2), A + L.x1 + r0 * D.h * e, part_f ? part_f + r0 * D.h * e : nullptr);
-  LAUNCH(MERAK_KC_GEMM_FWD, st, launch_gemm(dt, false, false, EPI_BIAS_RESID, &p, 1, st));
+  switch (k) {
+    case 0:  // LN1
+      LAUNCH(MERAK_KC_LN_FWD, st, launch_layernorm_fwd(dt, M, D.h, D.eps, x + r0 * D.h * e, P(params, S, l, P_LN1G),
+                                   P(params, S, l, P_LN1B), A + L.ln1 + r0 * D.h * e, (float*)(A + L.mu1) + r0,
+                                   (float*)(A + L.rs1) + r0, st));
+      break;
+    case 1:  // QKV (column parallel) + bias
+      *p = gp(M, 3 * D.hl, D.h, A + L.ln1 + r0 * D.h * e, D.h, P(params, S, l, P_WQKV), D.h,
+              A + L.qkv + r0 * 3 * D.hl * e, 3 * D.hl, P(params, S, l, P_BQKV));
+      *epi = EPI_BIAS;
+      break;
+    case 2:  // causal attention on the local heads
+      LAUNCH(MERAK_KC_ATTN_FWD, st, launch_attention_fwd(dt, D.bs, D.s, D.al, D.d, A + L.qkv + r0 * 3 * D.hl * e,
+                                     A + L.o + r0 * D.hl * e,
+                                     (float*)(A + L.lse) + (size_t)j * D.bs * D.al * D.s, st));
+      break;
+    case 3:  // projection (row parallel): partial sum -> hand-off; x1 = x + partial + b_o
+      *p = gp(M, D.h, D.hl, A + L.o + r0 * D.hl * e, D.hl, P(params, S, l, P_WO), D.hl, A + L.x1 + r0 * D.h * e, D.h,
+              P(params, S, l, P_BO), x + r0 * D.h * e, part_o ? part_o + r0 * D.h * e : nullptr);
+      *epi = EPI_BIAS_RESID;
+      break;
+    case 4:  // LN2
+      LAUNCH(MERAK_KC_LN_FWD, st, launch_layernorm_fwd(dt, M, D.h, D.eps, A + L.x1 + r0 * D.h * e,
+                                   P(params, S, l, P_LN2G), P(params, S, l, P_LN2B), A + L.ln2 + r0 * D.h * e,
+                                   (float*)(A + L.mu2) + r0, (float*)(A + L.rs2) + r0, st));
+      break;
+    case 5:  // FC1 (column parallel) + bias + GeLU; keeps the pre-activation u
+      *p = gp(M, D.fl, D.h, A + L.ln2 + r0 * D.h * e, D.h, P(params, S, l, P_W1), D.h, A + L.g + r0 * D.fl * e, D.fl,
+              P(params, S, l, P_B1), nullptr, A + L.u + r0 * D.fl * e);
+      *epi = EPI_BIAS_GELU;
+      break;
+    default:  // FC2 (row parallel): partial sum -> hand-off; y = x1 + partial + b2
+      *p = gp(M, D.h, D.fl, A + L.g + r0 * D.fl * e, D.fl, P(params, S, l, P_W2), D.fl, y + r0 * D.h * e, D.h,
+              P(params, S, l, P_B2), A + L.x1 + r0 * D.h * e, part_f ? part_f + r0 * D.h * e : nullptr);
+      *epi = EPI_BIAS_RESID;
+      break;
+  }
+  return MERAK_OK;
+}
+
+// Forward of block l over all sub-micro-batches: sub-micro-batch j runs on
+// stream j mod 2, issued step by step; the GEMMs of one step of the
+// sub-micro-batches that share a stream go out as one grouped launch (they are
+// independent problems of the same shape, so each keeps its own result).
+int block_forward(merak_stage* S, const void* params, int l, char* A, const char* x, char* y, char* part_o,
+                  char* part_f, hipStream_t s0, hipStream_t s1) {
+  const Dims& D = S->D;
+  for (int k = 0; k < kFwdSteps; ++k) {
+    for (int par = 0; par < 2; ++par) {
+      hipStream_t st = par ? s1 : s0;
+      GemmProblem probs[kMaxGroup];
+      int np = 0, epi = EPI_STORE;
+      for (int j = par; j < D.n; j += 2) {
+        TRY_INNER(block_forward_step(S, params, l, j, k, A, x, y, part_o, part_f, st, &probs[np], &epi));
+        if (fwd_step_is_gemm(k) && (++np == kMaxGroup || j + 2 >= D.n)) {
+          LAUNCH(MERAK_KC_GEMM_FWD, st, launch_gemm(D.dtype, false, false, epi, probs, np, st));
+          np = 0;
+        }
+      }
+    }
+  }
   return MERAK_OK;
 }
 
@@ -359,8 +400,10 @@ int block_forward(merak_stage* S, const void* params, int l, int j, char* A, con
 //   0 FC2 dX (+GeLU')  1 FC1 dX  2 LN2 bwd  3 proj dX  4 attention bwd
 //   5 QKV dX  6 LN1 bwd.
 constexpr int kChainSteps = 7;
+inline bool bwd_step_is_gemm(int k) { return k == 0 || k == 1 || k == 3 || k == 5; }
 int block_backward_step(merak_stage* S, const void* params, int l, int j, int k, const char* A, const char* x,
-                        const char* dy, char* dx, char* B, char* d_ln1, char* d_ln2, hipStream_t st) {
+                        const char* dy, char* dx, char* B, char* d_ln1, char* d_ln2, hipStream_t st, GemmProblem* gpr,
+                        int* epi) {
   const Dims& D = S->D;
   const ActLayout& L = S->W.act;
   const BwdLayout& Bl = S->W.bwd;
@@ -368,16 +411,15 @@ int block_backward_step(merak_stage* S, const void* params, int l, int j, int k,
   const size_t r0 = (size_t)j * D.Ms;
   const size_t e = D.esz;
   const int M = D.Ms;
-  GemmProblem p;
   switch (k) {
     case 0:  // FC2 backward: dg = dy W2; du = dg * gelu'(u)
-      p = gp(M, D.fl, D.h, dy + r0 * D.h * e, D.h, WT(S, l, 3), D.h, B + Bl.du + r0 * D.fl * e, D.fl, nullptr, nullptr,
-             (void*)(A + L.u + r0 * D.fl * e));
-      LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(dt, false, false, EPI_GELU_BWD, &p, 1, st));
+      *gpr = gp(M, D.fl, D.h, dy + r0 * D.h * e, D.h, WT(S, l, 3), D.h, B + Bl.du + r0 * D.fl * e, D.fl, nullptr,
+                nullptr, (void*)(A + L.u + r0 * D.fl * e));
+      *epi = EPI_GELU_BWD;
       break;
     case 1:  // FC1 backward: d_ln2 partial = du W1 (hand-off)
-      p = gp(M, D.h, D.fl, B + Bl.du + r0 * D.fl * e, D.fl, WT(S, l, 2), D.fl, d_ln2 + r0 * D.h * e, D.h);
-      LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(dt, false, false, EPI_STORE, &p, 1, st));
+      *gpr = gp(M, D.h, D.fl, B + Bl.du + r0 * D.fl * e, D.fl, WT(S, l, 2), D.fl, d_ln2 + r0 * D.h * e, D.h);
+      *epi = EPI_STORE;
       break;
     case 2:  // LN2 backward + residual gradient: dx1 = dy + LN2'(d_ln2)
       LAUNCH(MERAK_KC_LN_BWD, st, launch_layernorm_bwd(dt, M, D.h, d_ln2 + r0 * D.h * e, A + L.x1 + r0 * D.h * e,
@@ -385,8 +427,8 @@ int block_backward_step(merak_stage* S, const void* params, int l, int j, int k,
                                  P(params, S, l, P_LN2G), dy + r0 * D.h * e, B + Bl.dx1 + r0 * D.h * e, st));
       break;
     case 3:  // projection backward: dO = dx1 W_o
-      p = gp(M, D.hl, D.h, B + Bl.dx1 + r0 * D.h * e, D.h, WT(S, l, 1), D.h, B + Bl.dO + r0 * D.hl * e, D.hl);
-      LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(dt, false, false, EPI_STORE, &p, 1, st));
+      *gpr = gp(M, D.hl, D.h, B + Bl.dx1 + r0 * D.h * e, D.h, WT(S, l, 1), D.h, B + Bl.dO + r0 * D.hl * e, D.hl);
+      *epi = EPI_STORE;
       break;
     case 4: {  // attention backward -> dqkv
       const size_t lse_off = (size_t)j * D.bs * D.al * D.s;
@@ -397,9 +439,9 @@ int block_backward_step(merak_stage* S, const void* params, int l, int j, int k,
       break;
     }
     case 5:  // QKV backward: d_ln1 partial = dqkv W_qkv (hand-off)
-      p = gp(M, D.h, 3 * D.hl, B + Bl.dqkv + r0 * 3 * D.hl * e, 3 * D.hl, WT(S, l, 0), 3 * D.hl, d_ln1 + r0 * D.h * e,
-             D.h);
-      LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(dt, false, false, EPI_STORE, &p, 1, st));
+      *gpr = gp(M, D.h, 3 * D.hl, B + Bl.dqkv + r0 * 3 * D.hl * e, 3 * D.hl, WT(S, l, 0), 3 * D.hl,
+                d_ln1 + r0 * D.h * e, D.h);
+      *epi = EPI_STORE;
       break;
     default:  // LN1 backward + residual gradient: dx = dx1 + LN1'(d_ln1)
       LAUNCH(MERAK_KC_LN_BWD, st, launch_layernorm_bwd(dt, M, D.h, d_ln1 + r0 * D.h * e, x + r0 * D.h * e,
@@ -656,8 +698,7 @@ int merak_stage_fwd(merak_stage_t S, const void* params, const void* x, void* y,
     char* yout = (l == D.L - 1) ? (char*)y : block_input(S, l + 1);
     char* po = fwd_partials ? (char*)fwd_partials + (size_t)(2 * l) * th : nullptr;
     char* pf = fwd_partials ? (char*)fwd_partials + (size_t)(2 * l + 1) * th : nullptr;
-    for (int j = 0; j < D.n; ++j)
-      TRY(block_forward(S, params, l, j, A, xin, yout, po, pf, (j & 1) ? s1 : s0));
+    TRY(block_forward(S, params, l, A, xin, yout, po, pf, s0, s1));
   }
   TRY(join(S, s0, s1));
   return MERAK_OK;
@@ -676,8 +717,7 @@ int merak_stage_recompute(merak_stage_t S, const void* params, void* stream0, vo
     char* A = block_acts(S, l, 1);
     const char* xin = block_input(S, l);
     char* yout = S->ws + S->W.rc_y;  // the block output is already checkpointed
-    for (int j = 0; j < D.n; ++j)
-      TRY(block_forward(S, params, l, j, A, xin, yout, nullptr, nullptr, (j & 1) ? s1 : s0));
+    TRY(block_forward(S, params, l, A, xin, yout, nullptr, nullptr, s0, s1));
   }
   TRY(join(S, s0, s1));
   {
@@ -733,10 +773,21 @@ int merak_stage_bwd(merak_stage_t S, const void* params, const void* dy, void* d
     HIP_TRY(hipStreamWaitEvent(s1, S->ev_wt[l], 0));
     // Chains issued step by step over the sub-micro-batches (sub-micro-batch j
     // on stream j mod 2), so that the FFN weight gradients can start on the
-    // internal stream once every FC2 backward is done.
+    // internal stream once every FC2 backward is done.  The GEMMs of one step
+    // of the sub-micro-batches that share a stream form one grouped launch.
     for (int k = 0; k < kChainSteps; ++k) {
-      for (int j = 0; j < D.n; ++j)
-        TRY(block_backward_step(S, params, l, j, k, A, xin, dyl, dxl, B, d1, d2, (j & 1) ? s1 : s0));
+      for (int sp = 0; sp < 2; ++sp) {
+        hipStream_t st = sp ? s1 : s0;
+        GemmProblem probs[kMaxGroup];
+        int np = 0, epi = EPI_STORE;
+        for (int j = sp; j < D.n; j += 2) {
+          TRY(block_backward_step(S, params, l, j, k, A, xin, dyl, dxl, B, d1, d2, st, &probs[np], &epi));
+          if (bwd_step_is_gemm(k) && (++np == kMaxGroup || j + 2 >= D.n)) {
+            LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(D.dtype, false, false, epi, probs, np, st));
+            np = 0;
+          }
+        }
+      }
       if (k == 0 || k == kChainSteps - 1) {
         HIP_TRY(hipEventRecord(S->ev_j0, s0));
         HIP_TRY(hipEventRecord(S->ev_j1, s1));
