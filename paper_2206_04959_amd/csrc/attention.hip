@@ -111,6 +111,13 @@ __device__ __forceinline__ bf16x8_t frag_tr(const char* tile, int kb, int col0, 
 
 __device__ __forceinline__ bf16x8_t frag_kc(const bf16_t* p) { return *reinterpret_cast<const bf16x8_t*>(p); }
 
+// Sequence index of launch batch z when a launch covers several members (for
+// example the sub-micro-batches that share a stream), each of Bm consecutive
+// sequences, members mstride sequences apart.  Every tensor is addressed by
+// sequence (rows b * S + i, lse and delta rows (b * H + h) * S + i), so the
+// kernels need nothing else to work on such a group.
+__device__ __forceinline__ int seq_index(int z, int Bm, int mstride) { return (z / Bm) * mstride + z % Bm; }
+
 // LDS stages of the bf16 kernels (each four tiles: two 64-row blocks of two
 // tensors).  One stage keeps a workgroup small enough (53 KB at d = 96) to share
 // a CU with a GEMM workgroup of the other stream; the loads of the next block
@@ -131,14 +138,14 @@ constexpr size_t attn_lds_bytes() { return (size_t)kAttnStages * 4 * AttnTile<D>
 // Each stage holds the K and V tiles of two key blocks.
 // ---------------------------------------------------------------------------
 template <int D>
-__global__ void __launch_bounds__(256) attn_fwd_bf16(int S, int H, const bf16_t* __restrict__ qkv,
+__global__ void __launch_bounds__(256) attn_fwd_bf16(int S, int H, int Bm, int mstride, const bf16_t* __restrict__ qkv,
                                                      bf16_t* __restrict__ o, float* __restrict__ lse,
                                                      float scale_log2) {
   using TT = AttnTile<D>;
   constexpr int LD = TT::LD, KS = D / 16, DT = D / 32, TB = TT::BYTES;
   extern __shared__ __align__(16) char smem[];  // [stage][K blk a, K blk b, V blk a, V blk b]
 
-  const int b = blockIdx.z, hh = blockIdx.y;
+  const int b = seq_index(blockIdx.z, Bm, mstride), hh = blockIdx.y;
   const int qt = gridDim.x - 1 - blockIdx.x;  // longest rows first
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, l32 = lane & 31, hf = lane >> 5;
   const int qg = wave & 1, kh = wave >> 1;
@@ -287,12 +294,17 @@ __global__ void __launch_bounds__(256) attn_fwd_bf16(int S, int H, const bf16_t*
 // delta[b, h, i] = sum_d dO[b, i, h, d] * O[b, i, h, d]
 // ---------------------------------------------------------------------------
 template <typename T, int D>
-__global__ void __launch_bounds__(256) attn_delta_kernel(int B, int S, int H, const T* __restrict__ o,
-                                                         const T* __restrict__ dout, float* __restrict__ delta) {
-  const int row = blockIdx.x * 256 + threadIdx.x;  // (b, i, h) flattened
+__global__ void __launch_bounds__(256) attn_delta_kernel(int B, int S, int H, int Bm, int mstride,
+                                                         const T* __restrict__ o, const T* __restrict__ dout,
+                                                         float* __restrict__ delta) {
+  const int row = blockIdx.x * 256 + threadIdx.x;  // (launch batch, i, h) flattened
   if (row >= B * S * H) return;
-  const T* orow = o + (size_t)row * D;
-  const T* drow = dout + (size_t)row * D;
+  const int hh = row % H;
+  const int bi = row / H;
+  const int i = bi % S, b = seq_index(bi / S, Bm, mstride);
+  const size_t trow = ((size_t)b * S + i) * H + hh;
+  const T* orow = o + trow * D;
+  const T* drow = dout + trow * D;
   float s = 0.0f;
 #pragma unroll
   for (int c = 0; c < D; c += 8) {
@@ -302,9 +314,6 @@ __global__ void __launch_bounds__(256) attn_delta_kernel(int B, int S, int H, co
 #pragma unroll
     for (int e = 0; e < 8; ++e) s += a[e] * d[e];
   }
-  const int hh = row % H;
-  const int bi = row / H;
-  const int i = bi % S, b = bi / S;
   delta[((size_t)b * H + hh) * S + i] = s;
 }
 
@@ -316,7 +325,8 @@ __global__ void __launch_bounds__(256) attn_delta_kernel(int B, int S, int H, co
 // of two query blocks.  P is rebuilt from lse.
 // ---------------------------------------------------------------------------
 template <int D>
-__global__ void __launch_bounds__(256) attn_bwd_dkdv_bf16(int S, int H, const bf16_t* __restrict__ qkv,
+__global__ void __launch_bounds__(256) attn_bwd_dkdv_bf16(int S, int H, int Bm, int mstride,
+                                                          const bf16_t* __restrict__ qkv,
                                                           const bf16_t* __restrict__ dout,
                                                           const float* __restrict__ lse,
                                                           const float* __restrict__ delta,
@@ -327,7 +337,7 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_bf16(int S, int H, const bf
   extern __shared__ __align__(16) char smem[];  // [stage][Q a, Q b, dO a, dO b], then lse/delta
   float* vecs = reinterpret_cast<float*>(smem + kAttnStages * 4 * TB);  // [stage][lse a|b, delta a|b]
 
-  const int b = blockIdx.z, hh = blockIdx.y;
+  const int b = seq_index(blockIdx.z, Bm, mstride), hh = blockIdx.y;
   const int kt = blockIdx.x;  // early keys see the most queries: dispatched first
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, l32 = lane & 31, hf = lane >> 5;
   const int kg = wave & 1, qh = wave >> 1;
@@ -470,7 +480,8 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_bf16(int S, int H, const bf
 // stage, partial dQ sums added at the end.
 // ---------------------------------------------------------------------------
 template <int D>
-__global__ void __launch_bounds__(256) attn_bwd_dq_bf16(int S, int H, const bf16_t* __restrict__ qkv,
+__global__ void __launch_bounds__(256) attn_bwd_dq_bf16(int S, int H, int Bm, int mstride,
+                                                        const bf16_t* __restrict__ qkv,
                                                         const bf16_t* __restrict__ dout,
                                                         const float* __restrict__ lse,
                                                         const float* __restrict__ delta,
@@ -479,7 +490,7 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_bf16(int S, int H, const bf16
   constexpr int LD = TT::LD, KS = D / 16, DT = D / 32, TB = TT::BYTES;
   extern __shared__ __align__(16) char smem[];
 
-  const int b = blockIdx.z, hh = blockIdx.y;
+  const int b = seq_index(blockIdx.z, Bm, mstride), hh = blockIdx.y;
   const int qt = gridDim.x - 1 - blockIdx.x;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, l32 = lane & 31, hf = lane >> 5;
   const int qg = wave & 1, kh = wave >> 1;
@@ -708,14 +719,14 @@ __global__ void __launch_bounds__(128) attn_bwd_dkdv_f32(int B, int S, int H, co
 // Explicit instantiations of the bf16 kernels (the host pass then always emits
 // their launch stubs).
 #define MERAK_ATTN_INST(D)                                                                                        \
-  template __global__ void attn_fwd_bf16<D>(int, int, const bf16_t* __restrict__, bf16_t* __restrict__,          \
+  template __global__ void attn_fwd_bf16<D>(int, int, int, int, const bf16_t* __restrict__, bf16_t* __restrict__, \
                                             float* __restrict__, float);                                         \
-  template __global__ void attn_bwd_dkdv_bf16<D>(int, int, const bf16_t* __restrict__, const bf16_t* __restrict__, \
-                                                 const float* __restrict__, const float* __restrict__,           \
-                                                 bf16_t* __restrict__, float, float);                            \
-  template __global__ void attn_bwd_dq_bf16<D>(int, int, const bf16_t* __restrict__, const bf16_t* __restrict__,   \
-                                               const float* __restrict__, const float* __restrict__,             \
-                                               bf16_t* __restrict__, float, float);
+  template __global__ void attn_bwd_dkdv_bf16<D>(int, int, int, int, const bf16_t* __restrict__,                 \
+                                                 const bf16_t* __restrict__, const float* __restrict__,          \
+                                                 const float* __restrict__, bf16_t* __restrict__, float, float); \
+  template __global__ void attn_bwd_dq_bf16<D>(int, int, int, int, const bf16_t* __restrict__,                   \
+                                               const bf16_t* __restrict__, const float* __restrict__,            \
+                                               const float* __restrict__, bf16_t* __restrict__, float, float);
 MERAK_ATTN_INST(64)
 MERAK_ATTN_INST(96)
 MERAK_ATTN_INST(128)
@@ -732,29 +743,34 @@ static hipError_t allow_lds(K kern, size_t bytes, bool& done) {
 }
 
 template <int D>
-static hipError_t fwd_d(int dtype, int B, int S, int H, const void* qkv, void* o, float* lse, hipStream_t st) {
+static hipError_t fwd_d(int dtype, int B, int S, int H, int G, int mstride, const void* qkv, void* o, float* lse,
+                        hipStream_t st) {
   const float scale = 1.0f / sqrtf((float)D);
   if (dtype == DT_BF16) {
     constexpr size_t lds = attn_lds_bytes<D>();
     static bool ok = false;
     hipError_t e = allow_lds(attn_fwd_bf16<D>, lds, ok);
     if (e != hipSuccess) return e;
-    dim3 grid(S / 64, H, B);
-    hipLaunchKernelGGL((attn_fwd_bf16<D>), grid, dim3(256), lds, st, S, H, (const bf16_t*)qkv, (bf16_t*)o, lse,
-                       scale * kLog2e);
+    dim3 grid(S / 64, H, G * B);
+    hipLaunchKernelGGL((attn_fwd_bf16<D>), grid, dim3(256), lds, st, S, H, B, mstride, (const bf16_t*)qkv,
+                       (bf16_t*)o, lse, scale * kLog2e);
   } else {
-    dim3 grid((B * H * S + 127) / 128);
-    hipLaunchKernelGGL((attn_fwd_f32<D>), grid, dim3(128), 0, st, B, S, H, (const float*)qkv, (float*)o, lse,
-                       scale);
+    const size_t rs = (size_t)3 * H * D, seq_rows = (size_t)mstride * S;
+    for (int m = 0; m < G; ++m) {
+      dim3 grid((B * H * S + 127) / 128);
+      hipLaunchKernelGGL((attn_fwd_f32<D>), grid, dim3(128), 0, st, B, S, H,
+                         (const float*)qkv + m * seq_rows * rs, (float*)o + m * seq_rows * H * D,
+                         lse + m * seq_rows * H, scale);
+    }
   }
   return hipGetLastError();
 }
 
 template <int D>
-static hipError_t bwd_d(int dtype, int B, int S, int H, const void* qkv, const void* o, const float* lse,
-                        const void* dout, void* dqkv, float* delta, hipStream_t st) {
+static hipError_t bwd_d(int dtype, int B, int S, int H, int G, int mstride, const void* qkv, const void* o,
+                        const float* lse, const void* dout, void* dqkv, float* delta, hipStream_t st) {
   const float scale = 1.0f / sqrtf((float)D);
-  const int rows = B * S * H;
+  const int rows = G * B * S * H;
   if (dtype == DT_BF16) {
     constexpr size_t lds_q = attn_lds_bytes<D>();
     constexpr size_t lds_k = attn_lds_bytes<D>() + kAttnStages * 256 * sizeof(float);
@@ -763,45 +779,55 @@ static hipError_t bwd_d(int dtype, int B, int S, int H, const void* qkv, const v
     hipError_t e = allow_lds(attn_bwd_dkdv_bf16<D>, lds_k, ok_k);
     if (e == hipSuccess) e = allow_lds(attn_bwd_dq_bf16<D>, lds_q, ok_q);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((attn_delta_kernel<bf16_t, D>), dim3((rows + 255) / 256), dim3(256), 0, st, B, S, H,
-                       (const bf16_t*)o, (const bf16_t*)dout, delta);
-    dim3 grid(S / 64, H, B);
-    hipLaunchKernelGGL((attn_bwd_dkdv_bf16<D>), grid, dim3(256), lds_k, st, S, H, (const bf16_t*)qkv,
+    hipLaunchKernelGGL((attn_delta_kernel<bf16_t, D>), dim3((rows + 255) / 256), dim3(256), 0, st, G * B, S, H, B,
+                       mstride, (const bf16_t*)o, (const bf16_t*)dout, delta);
+    dim3 grid(S / 64, H, G * B);
+    hipLaunchKernelGGL((attn_bwd_dkdv_bf16<D>), grid, dim3(256), lds_k, st, S, H, B, mstride, (const bf16_t*)qkv,
                        (const bf16_t*)dout, lse, delta, (bf16_t*)dqkv, scale * kLog2e, scale);
-    hipLaunchKernelGGL((attn_bwd_dq_bf16<D>), grid, dim3(256), lds_q, st, S, H, (const bf16_t*)qkv,
+    hipLaunchKernelGGL((attn_bwd_dq_bf16<D>), grid, dim3(256), lds_q, st, S, H, B, mstride, (const bf16_t*)qkv,
                        (const bf16_t*)dout, lse, delta, (bf16_t*)dqkv, scale * kLog2e, scale);
   } else {
-    hipLaunchKernelGGL((attn_delta_kernel<float, D>), dim3((rows + 255) / 256), dim3(256), 0, st, B, S, H,
-                       (const float*)o, (const float*)dout, delta);
-    dim3 grid((B * H * S + 127) / 128);
-    hipLaunchKernelGGL((attn_bwd_dkdv_f32<D>), grid, dim3(128), 0, st, B, S, H, (const float*)qkv,
-                       (const float*)dout, lse, delta, (float*)dqkv, scale);
-    hipLaunchKernelGGL((attn_bwd_dq_f32<D>), grid, dim3(128), 0, st, B, S, H, (const float*)qkv,
-                       (const float*)dout, lse, delta, (float*)dqkv, scale);
+    hipLaunchKernelGGL((attn_delta_kernel<float, D>), dim3((rows + 255) / 256), dim3(256), 0, st, G * B, S, H, B,
+                       mstride, (const float*)o, (const float*)dout, delta);
+    const size_t rs = (size_t)3 * H * D, seq_rows = (size_t)mstride * S;
+    for (int m = 0; m < G; ++m) {
+      const float* q_m = (const float*)qkv + m * seq_rows * rs;
+      const float* do_m = (const float*)dout + m * seq_rows * H * D;
+      const float* lse_m = lse + m * seq_rows * H;
+      const float* del_m = delta + m * seq_rows * H;
+      float* dq_m = (float*)dqkv + m * seq_rows * rs;
+      dim3 grid((B * H * S + 127) / 128);
+      hipLaunchKernelGGL((attn_bwd_dkdv_f32<D>), grid, dim3(128), 0, st, B, S, H, q_m, do_m, lse_m, del_m, dq_m,
+                         scale);
+      hipLaunchKernelGGL((attn_bwd_dq_f32<D>), grid, dim3(128), 0, st, B, S, H, q_m, do_m, lse_m, del_m, dq_m,
+                         scale);
+    }
   }
   return hipGetLastError();
 }
 
 hipError_t launch_attention_fwd(int dtype, int batch, int seq, int heads, int d, const void* qkv, void* o,
-                                float* lse, hipStream_t stream) {
-  if (batch <= 0 || seq <= 0 || heads <= 0) return hipSuccess;
-  if (seq % 64 != 0) return hipErrorInvalidValue;
+                                float* lse, hipStream_t stream, int members, int member_stride) {
+  if (batch <= 0 || seq <= 0 || heads <= 0 || members <= 0) return hipSuccess;
+  if (seq % 64 != 0 || (members > 1 && member_stride < batch)) return hipErrorInvalidValue;
   switch (d) {
-    case 64: return fwd_d<64>(dtype, batch, seq, heads, qkv, o, lse, stream);
-    case 96: return fwd_d<96>(dtype, batch, seq, heads, qkv, o, lse, stream);
-    case 128: return fwd_d<128>(dtype, batch, seq, heads, qkv, o, lse, stream);
+    case 64: return fwd_d<64>(dtype, batch, seq, heads, members, member_stride, qkv, o, lse, stream);
+    case 96: return fwd_d<96>(dtype, batch, seq, heads, members, member_stride, qkv, o, lse, stream);
+    case 128: return fwd_d<128>(dtype, batch, seq, heads, members, member_stride, qkv, o, lse, stream);
     default: return hipErrorInvalidValue;
   }
 }
 
 hipError_t launch_attention_bwd(int dtype, int batch, int seq, int heads, int d, const void* qkv, const void* o,
-                                const float* lse, const void* dout, void* dqkv, float* delta, hipStream_t stream) {
-  if (batch <= 0 || seq <= 0 || heads <= 0) return hipSuccess;
-  if (seq % 64 != 0) return hipErrorInvalidValue;
+                                const float* lse, const void* dout, void* dqkv, float* delta, hipStream_t stream,
+                                int members, int member_stride) {
+  if (batch <= 0 || seq <= 0 || heads <= 0 || members <= 0) return hipSuccess;
+  if (seq % 64 != 0 || (members > 1 && member_stride < batch)) return hipErrorInvalidValue;
   switch (d) {
-    case 64: return bwd_d<64>(dtype, batch, seq, heads, qkv, o, lse, dout, dqkv, delta, stream);
-    case 96: return bwd_d<96>(dtype, batch, seq, heads, qkv, o, lse, dout, dqkv, delta, stream);
-    case 128: return bwd_d<128>(dtype, batch, seq, heads, qkv, o, lse, dout, dqkv, delta, stream);
+    case 64: return bwd_d<64>(dtype, batch, seq, heads, members, member_stride, qkv, o, lse, dout, dqkv, delta, stream);
+    case 96: return bwd_d<96>(dtype, batch, seq, heads, members, member_stride, qkv, o, lse, dout, dqkv, delta, stream);
+    case 128:
+      return bwd_d<128>(dtype, batch, seq, heads, members, member_stride, qkv, o, lse, dout, dqkv, delta, stream);
     default: return hipErrorInvalidValue;
   }
 }

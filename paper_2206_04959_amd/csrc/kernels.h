@@ -69,11 +69,14 @@ hipError_t launch_reduce_partials(int groups, int cols, const float* part, float
 hipError_t launch_transpose(int dtype, int rows, int cols, const void* src, int ld_src, void* dst, int ld_dst,
                             hipStream_t stream);
 
-// Causal attention on packed qkv [batch, seq, 3, heads, d].
+// Causal attention on packed qkv [batch, seq, 3, heads, d].  One launch may
+// cover `members` groups of `batch` sequences each, member m starting
+// m * member_stride sequences after the pointers given (so the sub-micro-
+// batches that share a stream form one grid); member_stride >= batch.
 hipError_t launch_attention_fwd(int dtype, int batch, int seq, int heads, int d, const void* qkv, void* o,
-                                float* lse, hipStream_t stream);
+                                float* lse, hipStream_t stream, int members = 1, int member_stride = 0);
 hipError_t launch_attention_bwd(int dtype, int batch, int seq, int heads, int d, const void* qkv,
                                 const void* o, const float* lse, const void* dout, void* dqkv,
-                                float* delta, hipStream_t stream);
+                                float* delta, hipStream_t stream, int members = 1, int member_stride = 0);
 
 }  // namespace merak

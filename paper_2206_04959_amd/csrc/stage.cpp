@@ -321,11 +321,12 @@ GemmProblem gp(int M, int N, int K, const void* a, int lda, const void* b, int l
 //   0 LN1  1 QKV GEMM  2 attention  3 projection GEMM  4 LN2  5 FC1 GEMM
 //   6 FC2 GEMM.
 // GEMM steps only describe their problem (*p, *epi) for a grouped launch; the
-// other steps are launched on st.
+// other steps are launched on st.  The attention step covers `members`
+// sub-micro-batches j, j + 2, ... in one launch.
 constexpr int kFwdSteps = 7;
 inline bool fwd_step_is_gemm(int k) { return k == 1 || k == 3 || k == 5 || k == 6; }
 int block_forward_step(merak_stage* S, const void* params, int l, int j, int k, char* A, const char* x, char* y,
-                       char* part_o, char* part_f, hipStream_t st, GemmProblem* p, int* epi) {
+                       char* part_o, char* part_f, hipStream_t st, GemmProblem* p, int* epi, int members) {
   const Dims& D = S->D;
   const ActLayout& L = S->W.act;
   const int dt = D.dtype;
@@ -346,7 +347,8 @@ int block_forward_step(merak_stage* S, const void* params, int l, int j, int k, 
     case 2:  // causal attention on the local heads
       LAUNCH(MERAK_KC_ATTN_FWD, st, launch_attention_fwd(dt, D.bs, D.s, D.al, D.d, A + L.qkv + r0 * 3 * D.hl * e,
                                      A + L.o + r0 * D.hl * e,
-                                     (float*)(A + L.lse) + (size_t)j * D.bs * D.al * D.s, st));
+                                     (float*)(A + L.lse) + (size_t)j * D.bs * D.al * D.s, st, members,
+                                     2 * D.bs));
       break;
     case 3:  // projection (row parallel): partial sum -> hand-off; x1 = x + partial + b_o
       *p = gp(M, D.h, D.hl, A + L.o + r0 * D.hl * e, D.hl, P(params, S, l, P_WO), D.hl, A + L.x1 + r0 * D.h * e, D.h,
@@ -384,8 +386,10 @@ int block_forward(merak_stage* S, const void* params, int l, char* A, const char
       hipStream_t st = par ? s1 : s0;
       GemmProblem probs[kMaxGroup];
       int np = 0, epi = EPI_STORE;
+      const int members = (D.n - par + 1) / 2;  // sub-micro-batches on this stream
       for (int j = par; j < D.n; j += 2) {
-        TRY_INNER(block_forward_step(S, params, l, j, k, A, x, y, part_o, part_f, st, &probs[np], &epi));
+        if (k == 2 && j != par) break;  // one attention launch covers the stream's sub-micro-batches
+        TRY_INNER(block_forward_step(S, params, l, j, k, A, x, y, part_o, part_f, st, &probs[np], &epi, members));
         if (fwd_step_is_gemm(k) && (++np == kMaxGroup || j + 2 >= D.n)) {
           LAUNCH(MERAK_KC_GEMM_FWD, st, launch_gemm(D.dtype, false, false, epi, probs, np, st));
           np = 0;
@@ -399,11 +403,13 @@ int block_forward(merak_stage* S, const void* params, int l, char* A, const char
 // Step k (0..6) of the input-gradient chain of block l for sub-micro-batch j:
 //   0 FC2 dX (+GeLU')  1 FC1 dX  2 LN2 bwd  3 proj dX  4 attention bwd
 //   5 QKV dX  6 LN1 bwd.
+// GEMM steps only describe their problem for a grouped launch; the attention
+// step covers `members` sub-micro-batches j, j + 2, ... in one launch.
 constexpr int kChainSteps = 7;
 inline bool bwd_step_is_gemm(int k) { return k == 0 || k == 1 || k == 3 || k == 5; }
 int block_backward_step(merak_stage* S, const void* params, int l, int j, int k, const char* A, const char* x,
                         const char* dy, char* dx, char* B, char* d_ln1, char* d_ln2, hipStream_t st, GemmProblem* gpr,
-                        int* epi) {
+                        int* epi, int members) {
   const Dims& D = S->D;
   const ActLayout& L = S->W.act;
   const BwdLayout& Bl = S->W.bwd;
@@ -435,7 +441,7 @@ int block_backward_step(merak_stage* S, const void* params, int l, int j, int k,
       LAUNCH(MERAK_KC_ATTN_BWD, st, launch_attention_bwd(dt, D.bs, D.s, D.al, D.d, A + L.qkv + r0 * 3 * D.hl * e,
                                    A + L.o + r0 * D.hl * e, (const float*)(A + L.lse) + lse_off,
                                    B + Bl.dO + r0 * D.hl * e, B + Bl.dqkv + r0 * 3 * D.hl * e,
-                                   (float*)(B + Bl.delta) + lse_off, st));
+                                   (float*)(B + Bl.delta) + lse_off, st, members, 2 * D.bs));
       break;
     }
     case 5:  // QKV backward: d_ln1 partial = dqkv W_qkv (hand-off)
@@ -780,8 +786,10 @@ int merak_stage_bwd(merak_stage_t S, const void* params, const void* dy, void* d
         hipStream_t st = sp ? s1 : s0;
         GemmProblem probs[kMaxGroup];
         int np = 0, epi = EPI_STORE;
+        const int members = (D.n - sp + 1) / 2;  // sub-micro-batches on this stream
         for (int j = sp; j < D.n; j += 2) {
-          TRY(block_backward_step(S, params, l, j, k, A, xin, dyl, dxl, B, d1, d2, st, &probs[np], &epi));
+          if (k == 4 && j != sp) break;  // one attention launch covers the stream's sub-micro-batches
+          TRY(block_backward_step(S, params, l, j, k, A, xin, dyl, dxl, B, d1, d2, st, &probs[np], &epi, members));
           if (bwd_step_is_gemm(k) && (++np == kMaxGroup || j + 2 >= D.n)) {
             LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(D.dtype, false, false, epi, probs, np, st));
             np = 0;

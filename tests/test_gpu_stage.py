@@ -25,6 +25,10 @@ SMALL = {
                                  x_std=1.0, seed=33),
     "d128-t4-bf16": synth.StageShape("d128", n_blocks=2, hidden=1024, n_heads=8, ffn=4096, seq_len=128,
                                      micro_batch=4, tp_degree=4, n_sub=4, recompute_mask=0b11, seed=34),
+    # three sub-micro-batches: the two streams carry two and one of them, so
+    # the per-stream grouped launches have unequal member counts
+    "d64-n3-bf16": synth.StageShape("d64n3", n_blocks=2, hidden=256, n_heads=4, ffn=1024, seq_len=128,
+                                    micro_batch=6, tp_degree=1, n_sub=3, recompute_mask=0b10, seed=35),
 }
 
 
@@ -55,6 +59,17 @@ def test_sub_micro_batch_split_and_streams_do_not_change_results():
         got = StageRun(base.replace(n_sub=n), streams=streams).run().raw()
         for k in ref:
             assert np.array_equal(ref[k], got[k]), (n, streams, k)
+
+
+def test_grouped_launches_do_not_change_results():
+    """Sub-micro-batch counts whose per-stream groups hold 1, 2 or 3 members
+    (grouped GEMM and attention launches) give the unsplit bits."""
+    base = SMALL["d64-n3-bf16"]
+    ref = StageRun(base.replace(n_sub=1), streams=1).run().raw()
+    for n in (2, 3, 6):
+        got = StageRun(base.replace(n_sub=n)).run().raw()
+        for k in ref:
+            assert np.array_equal(ref[k], got[k]), (n, k)
 
 
 def test_runs_are_deterministic_and_accumulate_adds():
