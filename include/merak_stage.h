@@ -265,6 +265,58 @@ int merak_schedule_simulate(int kind, int n_stages, int n_micro, double cost_fwd
                             double* makespan, double* busy);
 
 /* ------------------------------------------------------------------------
+ * Graph sharding (paper Sec. 4.2, Alg. 1 "Search Node Dependency" and Alg. 2
+ * "Graph-Sharding").  Host-only, no GPU.
+ *
+ * Splits a model's dataflow graph into a sequence of subgraphs that run one
+ * after the other, so that consecutive runs of the sequence can be assigned to
+ * pipeline stages.  Nodes are visited in topological order; a node joins the
+ * subgraph of its farthest dependency (a graph input's first user, the
+ * subgraph after the one whose output it reads, or the subgraph of any other
+ * earlier node except the last visited one), pulling the nodes visited since
+ * that dependency along; common nodes (cheap values used all over the graph,
+ * such as a causal mask) are no dependency.  A subgraph closes once its
+ * parameters exceed sum(params) / k; its outputs are the closing node plus the
+ * visited common nodes that still have uses left.
+ *
+ * Readings where the paper is silent: a node reading a graph input twice is
+ * no dependency of itself; the dependency node itself keeps its
+ * subgraph when later nodes join it; reopening a subgraph drops the outputs
+ * recorded for it and for every later subgraph; the last subgraph is emitted
+ * even if it never closed, with the graph outputs as its outputs; a
+ * subgraph's inputs are the previous subgraph's outputs plus the graph inputs
+ * whose first user it holds.
+ *
+ * Graph (n_nodes nodes in topological order, graph inputs included):
+ *   kind[i]         MERAK_NODE_COMPUTE, MERAK_NODE_INPUT (a graph input: no
+ *                   arguments, not assigned to a subgraph) or MERAK_NODE_COMMON;
+ *   params[i]       parameters the node holds (>= 0);
+ *   arg_ptr[0..n_nodes], arg_idx[]: node i's arguments are
+ *                   arg_idx[arg_ptr[i] .. arg_ptr[i+1]), one entry per use,
+ *                   each an index < i;
+ *   common_uses[i]  for common nodes, how many argument entries name it;
+ *   graph_outputs[0..n_outputs-1]: node indices the graph returns;
+ *   k               requested number of subgraphs (>= 1).
+ * Result:
+ *   subgraph_of[i]  subgraph id of node i (-1 for graph inputs);
+ *   *n_subgraphs;
+ *   io_ptr[0..2 * n_nodes], io_idx[0..io_capacity-1]: subgraph j's inputs are
+ *   io_idx[io_ptr[2j] .. io_ptr[2j+1]) and its outputs io_idx[io_ptr[2j+1] ..
+ *   io_ptr[2j+2]) (node indices).
+ * Errors: MERAK_ERR_INVALID_ARG (null pointers, n_nodes < 1, k < 1, an
+ * argument index not smaller than its node's, a graph input with arguments,
+ * an unknown kind, negative params or uses), MERAK_ERR_WORKSPACE if io_idx
+ * is too small (*n_subgraphs is still set; io_ptr[2 * *n_subgraphs] then
+ * holds the capacity needed).  Nothing else is written on an argument error.
+ * ---------------------------------------------------------------------- */
+typedef enum { MERAK_NODE_COMPUTE = 0, MERAK_NODE_INPUT = 1, MERAK_NODE_COMMON = 2 } merak_node_kind;
+
+int merak_graph_shard(int n_nodes, const int32_t* kind, const int64_t* params, const int32_t* arg_ptr,
+                      const int32_t* arg_idx, const int32_t* common_uses, int n_outputs,
+                      const int32_t* graph_outputs, int k, int32_t* subgraph_of, int32_t* n_subgraphs,
+                      int32_t* io_ptr, int32_t* io_idx, int io_capacity);
+
+/* ------------------------------------------------------------------------
  * Per-kernel entry points (each launches one hot-path kernel on `stream`).
  * They exist so each kernel can be checked and timed on its own; the stage
  * calls above use the same kernels.  dtype is merak_dtype; pointers follow the

@@ -60,6 +60,7 @@ _SIGS = {
     "merak_schedule_stage": ([_I, _I, _I, _I, _P, _I, ctypes.POINTER(_I)], _I),
     "merak_schedule_simulate": ([_I, _I, _I, ctypes.c_double, ctypes.c_double, ctypes.c_double,
                                  ctypes.POINTER(ctypes.c_double), _P], _I),
+    "merak_graph_shard": ([_I, _P, _P, _P, _P, _P, _I, _P, _I, _P, ctypes.POINTER(ctypes.c_int32), _P, _P, _I], _I),
     "merak_plan_alpha1": ([_I, ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_double,
                            ctypes.POINTER(ctypes.c_double)], _I),
     "merak_layernorm_fwd": ([_I, _I, _I, _F, _P, _P, _P, _P, _P, _P, _P], _I),

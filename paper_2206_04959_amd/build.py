@@ -17,7 +17,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libmerak_stage.so")
-SOURCES = ("gemm.hip", "attention.hip", "norm.hip", "stage.cpp")
+SOURCES = ("gemm.hip", "attention.hip", "norm.hip", "stage.cpp", "graph_shard.cpp")
 
 ARCH = "gfx950"
 # Packed fp32 instructions are kept out of every code object.
