@@ -398,47 +398,45 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_bf16(int S, int H, int Bm, 
     const float* lse_s = vecs + cur * 256 + qh * 64;
     const float* del_s = lse_s + 128;
 
-    f32x16_t p[2], dp[2];
-#pragma unroll
-    for (int t = 0; t < 2; ++t) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) p[t][r] = dp[t][r] = 0.0f;
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        p[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_row<LD>(Qt, t * 32 + l32, ks * 16 + hf * 8), kf[ks], p[t],
-                                                       0, 0, 0);
-        dp[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_row<LD>(dOt, t * 32 + l32, ks * 16 + hf * 8), vf[ks],
-                                                        dp[t], 0, 0, 0);
-      }
-    }
-    // p[t][r]: query qs + t*32 + (r/4)*8 + 4*hf + r%4, key `key`.
+    // The two 32-query halves of the block one after the other (smaller live
+    // register set); each dK/dV accumulator still takes its four 16-query
+    // groups in order 0..3, so the sums are those of the whole block.
     const bool diag = qs < kw0 + 32;  // some query of the block precedes some key of the wave
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+    for (int t = 0; t < 2; ++t) {
+      f32x16_t p, dp;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) p[r] = dp[r] = 0.0f;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        p = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_row<LD>(Qt, t * 32 + l32, ks * 16 + hf * 8), kf[ks], p, 0,
+                                                    0, 0);
+        dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_row<LD>(dOt, t * 32 + l32, ks * 16 + hf * 8), vf[ks], dp,
+                                                     0, 0, 0);
+      }
+      // p[r]: query qs + t*32 + (r/4)*8 + 4*hf + r%4, key `key`.
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int qi = t * 32 + (r >> 2) * 8 + hf * 4 + (r & 3);
-        float pv = __builtin_amdgcn_exp2f(p[t][r] * scale_log2 - lse_s[qi] * kLog2e);
+        float pv = __builtin_amdgcn_exp2f(p[r] * scale_log2 - lse_s[qi] * kLog2e);
         if (diag && key > qs + qi) pv = 0.0f;
-        p[t][r] = pv;
-        dp[t][r] = pv * (dp[t][r] - del_s[qi]);
+        p[r] = pv;
+        dp[r] = pv * (dp[r] - del_s[qi]);
       }
-    bf16x8_t pb[4], sb[4];
+      const bf16x8_t pb[2] = {cvt8(p, 0), cvt8(p, 8)};
+      const bf16x8_t sb[2] = {cvt8(dp, 0), cvt8(dp, 8)};
+      // dV^T[d][key] += dO^T[d][q] P[q][key];  dK^T[d][key] += Q^T[d][q] dS[q][key]
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      pb[g] = cvt8(p[g >> 1], (g & 1) * 8);
-      sb[g] = cvt8(dp[g >> 1], (g & 1) * 8);
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int gg = 0; gg < 2; ++gg) {
+          const int g = 2 * t + gg;
+          dv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_tr<LD>(dOt, g * 16, dt * 32, lane), pb[gg], dv[dt],
+                                                           0, 0, 0);
+          dk[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_tr<LD>(Qt, g * 16, dt * 32, lane), sb[gg], dk[dt],
+                                                           0, 0, 0);
+        }
     }
-    // dV^T[d][key] += dO^T[d][q] P[q][key];  dK^T[d][key] += Q^T[d][q] dS[q][key]
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        dv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_tr<LD>(dOt, g * 16, dt * 32, lane), pb[g], dv[dt], 0, 0,
-                                                         0);
-        dk[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_tr<LD>(Qt, g * 16, dt * 32, lane), sb[g], dk[dt], 0, 0,
-                                                         0);
-      }
   }
 
   // Add the two query halves.
