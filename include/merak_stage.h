@@ -157,7 +157,12 @@ int merak_stage_fwd(merak_stage_t stage, const void* params, const void* x, void
  * bit-identical to what the forward pass computed.  Needs no upstream gradient
  * (early recomputation).  MERAK_ERR_ORDER if no forward pass is pending.  A
  * no-op (MERAK_OK) when the mask is 0.  params must hold the same values as in
- * the forward call. */
+ * the forward call.
+ * The streams may differ from the ones the backward will use: the backward of
+ * each recomputed block waits for that block's recomputation only, so the
+ * recomputation of the first blocks can overlap the backward of the later
+ * ones (which the backward reaches first).  The caller orders these streams
+ * after the forward pass (the block inputs are its results). */
 int merak_stage_recompute(merak_stage_t stage, const void* params, void* stream0, void* stream1);
 
 /* Backward pass of the stage for the pending micro-batch.

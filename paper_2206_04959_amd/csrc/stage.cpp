@@ -228,6 +228,7 @@ struct merak_stage {
   hipStream_t aux;
   hipEvent_t ev_fork, ev_s1, ev_j0, ev_j1, ev_aux, ev_dw[2];
   hipEvent_t ev_wt[kMaxBlocks];  // transposed weights of block l ready
+  hipEvent_t ev_rc[kMaxBlocks][2];  // recompute of block l done on its two streams
   int state;  // 0 idle, 1 forward pending, 2 recomputed
   const void* x0;
   // optional per-launch event timing of one kernel class
@@ -619,14 +620,28 @@ int merak_stage_create(const merak_stage_config* cfg, void* workspace, size_t wo
     e = hipEventCreateWithFlags(ev, hipEventDisableTiming);
     if (e == hipSuccess) ++made;
   }
-  int made_wt = 0;
+  int made_wt = 0, made_rc = 0;
   for (int l = 0; l < D.L && e == hipSuccess; ++l) {
     e = hipEventCreateWithFlags(&S->ev_wt[l], hipEventDisableTiming);
     if (e == hipSuccess) ++made_wt;
   }
+  for (int l = 0; l < D.L && e == hipSuccess; ++l) {
+    e = hipEventCreateWithFlags(&S->ev_rc[l][0], hipEventDisableTiming);
+    if (e != hipSuccess) break;
+    e = hipEventCreateWithFlags(&S->ev_rc[l][1], hipEventDisableTiming);
+    if (e != hipSuccess) {
+      (void)hipEventDestroy(S->ev_rc[l][0]);
+      break;
+    }
+    ++made_rc;
+  }
   if (e != hipSuccess) {
     for (int i = 0; i < made; ++i) (void)hipEventDestroy(*evs[i]);
     for (int l = 0; l < made_wt; ++l) (void)hipEventDestroy(S->ev_wt[l]);
+    for (int l = 0; l < made_rc; ++l) {
+      (void)hipEventDestroy(S->ev_rc[l][0]);
+      (void)hipEventDestroy(S->ev_rc[l][1]);
+    }
     if (have_stream) (void)hipStreamDestroy(S->aux);
     delete S;
     return MERAK_ERR_HIP;
@@ -644,7 +659,11 @@ int merak_stage_destroy(merak_stage_t S) {
   }
   hipEvent_t evs[] = {S->ev_fork, S->ev_s1, S->ev_j0, S->ev_j1, S->ev_aux, S->ev_dw[0], S->ev_dw[1]};
   for (hipEvent_t ev : evs) (void)hipEventDestroy(ev);
-  for (int l = 0; l < S->D.L; ++l) (void)hipEventDestroy(S->ev_wt[l]);
+  for (int l = 0; l < S->D.L; ++l) {
+    (void)hipEventDestroy(S->ev_wt[l]);
+    (void)hipEventDestroy(S->ev_rc[l][0]);
+    (void)hipEventDestroy(S->ev_rc[l][1]);
+  }
   for (hipEvent_t ev : S->t_ev) (void)hipEventDestroy(ev);
   (void)hipStreamDestroy(S->aux);
   delete S;
@@ -724,6 +743,9 @@ int merak_stage_recompute(merak_stage_t S, const void* params, void* stream0, vo
     const char* xin = block_input(S, l);
     char* yout = S->ws + S->W.rc_y;  // the block output is already checkpointed
     TRY(block_forward(S, params, l, A, xin, yout, nullptr, nullptr, s0, s1));
+    // the backward of block l waits for these (it may run on other streams)
+    HIP_TRY(hipEventRecord(S->ev_rc[l][0], s0));
+    HIP_TRY(hipEventRecord(S->ev_rc[l][1], s1));
   }
   TRY(join(S, s0, s1));
   {
@@ -777,6 +799,13 @@ int merak_stage_bwd(merak_stage_t S, const void* params, const void* dy, void* d
     }
     HIP_TRY(hipStreamWaitEvent(s0, S->ev_wt[l], 0));
     HIP_TRY(hipStreamWaitEvent(s1, S->ev_wt[l], 0));
+    if ((D.mask >> l) & 1) {  // the activations recomputed for this block
+      for (int q = 0; q < 2; ++q) {
+        HIP_TRY(hipStreamWaitEvent(s0, S->ev_rc[l][q], 0));
+        HIP_TRY(hipStreamWaitEvent(s1, S->ev_rc[l][q], 0));
+        HIP_TRY(hipStreamWaitEvent(S->aux, S->ev_rc[l][q], 0));
+      }
+    }
     // Chains issued step by step over the sub-micro-batches (sub-micro-batch j
     // on stream j mod 2), so that the FFN weight gradients can start on the
     // internal stream once every FC2 backward is done.  The GEMMs of one step

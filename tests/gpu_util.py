@@ -31,7 +31,7 @@ def tol_for(shape) -> float:
 class StageRun:
     """Inputs on the device plus the outputs of one fwd -> recompute -> bwd call sequence."""
 
-    def __init__(self, shape, streams=2, with_partials=True, stage=None):
+    def __init__(self, shape, streams=2, with_partials=True, stage=None, rc_streams=False):
         torch = need_gpu()
         self.shape = shape
         self.cfg = B.make_config(shape)
@@ -56,6 +56,8 @@ class StageRun:
         else:
             s = torch.cuda.Stream()
             self.streams = (s, s)
+        # recomputation on streams of its own, overlapping the backward
+        self.rc_streams = (torch.cuda.Stream(), torch.cuda.Stream()) if rc_streams else self.streams
         self.torch = torch
 
     def run(self, accumulate=False):
@@ -63,7 +65,9 @@ class StageRun:
         s0 = self.streams[0]
         s0.wait_stream(torch.cuda.current_stream())
         self.stage.fwd(self.params, self.x, self.y, self.fp, streams=self.streams)
-        self.stage.recompute(self.params, streams=self.streams)
+        for r in self.rc_streams:
+            r.wait_stream(s0)  # the forward's block inputs
+        self.stage.recompute(self.params, streams=self.rc_streams)
         self.stage.bwd(self.params, self.dy, self.dx, self.grads, accumulate, self.bp, streams=self.streams)
         torch.cuda.current_stream().wait_stream(s0)
         torch.cuda.synchronize()

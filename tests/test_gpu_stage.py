@@ -52,6 +52,16 @@ def test_recompute_gives_bit_identical_gradients():
         assert np.array_equal(a[k], b[k]), k
 
 
+def test_recompute_on_its_own_streams_overlapping_the_backward():
+    """Recomputation issued on other streams than the backward (the backward
+    of each recomputed block waits for that block only) gives the same bits."""
+    base = SMALL["d64-t2-bf16"].replace(recompute_mask=0b011)
+    a = StageRun(base).run().raw()
+    b = StageRun(base, rc_streams=True).run().raw()
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
+
+
 def test_sub_micro_batch_split_and_streams_do_not_change_results():
     base = SMALL["d64-t2-bf16"]
     ref = StageRun(base.replace(n_sub=1), streams=1).run().raw()
