@@ -3,8 +3,8 @@
 
 One step = forward + recompute + backward of one GPU's share of a GPT pipeline
 stage for one micro-batch (every step of the hot path), run through the C ABI
-of the HIP library: forward and backward on two streams, the recomputation on
-two more, overlapping the backward of the blocks that keep their activations.  Default workload: the 8.3B-shaped shard at
+of the HIP library: forward, recomputation and backward on two streams (the
+library adds a third for the weight gradients).  Default workload: the 8.3B-shaped shard at
 tensor-parallel degree 4 (6 blocks, hidden 3072, 32 heads / 8 local, FFN 12288
 / 3072 local, seq 1024, micro-batch 8 in 4 sub-micro-batches, recompute on 3
 of 6 blocks, bf16).  Inputs are seeded synthetic tensors already resident in
@@ -123,19 +123,16 @@ def main() -> int:
     log(f"[bench] workspace {stage.workspace_bytes / 2**30:.2f} GiB, recompute area "
         f"{stage.recompute_bytes / 2**30:.2f} GiB")
     s0, s1 = torch.cuda.Stream(), torch.cuda.Stream()
-    r0, r1 = torch.cuda.Stream(), torch.cuda.Stream()  # recomputation (early, overlapping the backward)
     s0.wait_stream(torch.cuda.current_stream())
     torch.cuda.synchronize()
 
     def step():
         stage.fwd(params, x, y, fwd_part, streams=(s0, s1))
-        # The recomputed blocks are the first ones, which the backward reaches
-        # last: their recomputation runs on streams of its own while the
-        # backward of the later blocks proceeds (each recomputed block's
-        # backward waits for its own recomputation inside the library).
-        r0.wait_stream(s0)
-        r1.wait_stream(s0)
-        stage.recompute(params, streams=(r0, r1))
+        # Recomputation on the backward's own streams, issued ahead of it.
+        # Streams of its own, running beside the backward of the blocks that
+        # kept their activations, measured slower: the step is throughput-
+        # bound, and the extra co-running kernels cost more than they fill.
+        stage.recompute(params, streams=(s0, s1))
         stage.bwd(params, dy, dx, grads, False, bwd_part, streams=(s0, s1))
 
     for _ in range(args.warmup):

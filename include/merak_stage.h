@@ -196,8 +196,7 @@ typedef enum {
   MERAK_KC_LN_BWD = 7,     /* LayerNorm backward (input gradient)                        */
   MERAK_KC_REDUCE = 8,     /* bias / LayerNorm parameter gradient reductions             */
   MERAK_KC_GEMM_DW_ATTN = 9, /* weight-gradient GEMMs of QKV and projection, one per block */
-  MERAK_KC_TRANSPOSE = 10, /* weight transposes for the backward's input-gradient GEMMs    */
-  MERAK_KC_COUNT = 11
+  MERAK_KC_COUNT = 10
 } merak_kernel_class;
 
 /* Measurement aid: from now on, bracket every launch of `kernel_class` made by

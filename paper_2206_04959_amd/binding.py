@@ -24,7 +24,7 @@ STATUS = {0: "MERAK_OK", -1: "MERAK_ERR_INVALID_ARG", -2: "MERAK_ERR_SHAPE", -3:
 
 EPI_STORE, EPI_BIAS, EPI_BIAS_GELU, EPI_BIAS_RESID, EPI_GELU_BWD, EPI_F32 = range(6)
 (KC_NONE, KC_GEMM_FWD, KC_GEMM_DX, KC_GEMM_DW, KC_ATTN_FWD, KC_ATTN_BWD, KC_LN_FWD, KC_LN_BWD,
- KC_REDUCE, KC_GEMM_DW_ATTN, KC_TRANSPOSE) = range(11)
+ KC_REDUCE, KC_GEMM_DW_ATTN) = range(10)
 
 
 class MerakError(RuntimeError):

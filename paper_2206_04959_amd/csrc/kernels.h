@@ -39,9 +39,12 @@ constexpr int kMaxGroup = 4;
 hipError_t launch_gemm(int dtype, bool a_t, bool b_t, int epi, const GemmProblem* probs, int n_probs,
                        hipStream_t stream);
 
-// LayerNorm over rows of width h (h % 8 == 0).
+// LayerNorm over rows of width h (h % 8 == 0).  Like attention, one launch may
+// cover `members` groups of `rows` rows, member m starting m * member_stride
+// rows after every row-indexed pointer given (member_stride >= rows).
 hipError_t launch_layernorm_fwd(int dtype, int rows, int h, float eps, const void* x, const void* gamma,
-                                const void* beta, void* y, float* mean, float* rstd, hipStream_t stream);
+                                const void* beta, void* y, float* mean, float* rstd, hipStream_t stream,
+                                int members = 1, int member_stride = 0);
 
 // Rows per partial-sum segment of the deterministic column reductions.
 constexpr int kReduceRows = 64;
@@ -50,7 +53,8 @@ inline size_t reduce_groups(int rows) { return (size_t)(rows + kReduceRows - 1) 
 // dx = dres + LN'(dout) (input gradient of LayerNorm plus the residual gradient).
 hipError_t launch_layernorm_bwd(int dtype, int rows, int h, const void* dout, const void* x,
                                 const float* mean, const float* rstd, const void* gamma,
-                                const void* dres, void* dx, hipStream_t stream);
+                                const void* dres, void* dx, hipStream_t stream, int members = 1,
+                                int member_stride = 0);
 
 // Partials [reduce_groups(rows), h] of sum(dout * xhat) and sum(dout).
 hipError_t launch_layernorm_param_partials(int dtype, int rows, int h, const void* dout, const void* x,
@@ -64,10 +68,6 @@ hipError_t launch_column_partials(int dtype, int rows, int cols, const void* x, 
 // out[c] (=|+=) sum over groups g of part[g, c], in increasing g.
 hipError_t launch_reduce_partials(int groups, int cols, const float* part, float* out, int accumulate,
                                   hipStream_t stream);
-
-// dst[c, r] = src[r, c] for a [rows, cols] matrix (rows, cols multiples of 64).
-hipError_t launch_transpose(int dtype, int rows, int cols, const void* src, int ld_src, void* dst, int ld_dst,
-                            hipStream_t stream);
 
 // Causal attention on packed qkv [batch, seq, 3, heads, d].  One launch may
 // cover `members` groups of `batch` sequences each, member m starting

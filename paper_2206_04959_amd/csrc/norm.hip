@@ -17,14 +17,23 @@ namespace merak {
 
 constexpr int kRowsPerBlock = 4;  // waves per 256-thread workgroup
 
+// Rows of a launch may come from `members` equal groups of mrows rows, group m
+// starting m * mstride rows after the pointers given: logical row r is
+// physical row (r / mrows) * mstride + r % mrows.
+__device__ __forceinline__ int member_row(int r, int mrows, int mstride) {
+  return (r / mrows) * mstride + r % mrows;
+}
+
 template <typename T, int CH>
-__global__ void __launch_bounds__(256) ln_fwd_kernel(int rows, int h, float eps, const T* __restrict__ x,
+__global__ void __launch_bounds__(256) ln_fwd_kernel(int rows, int mrows, int mstride, int h, float eps,
+                                                     const T* __restrict__ x,
                                                      const T* __restrict__ gamma, const T* __restrict__ beta,
                                                      T* __restrict__ y, float* __restrict__ mean,
                                                      float* __restrict__ rstd) {
-  const int row = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+  const int lrow = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  if (row >= rows) return;
+  if (lrow >= rows) return;
+  const int row = member_row(lrow, mrows, mstride);
   const T* xr = x + (size_t)row * h;
   float v[CH][8];
   float s = 0.0f;
@@ -74,13 +83,15 @@ __global__ void __launch_bounds__(256) ln_fwd_kernel(int rows, int h, float eps,
 // dx = dres + rstd * (dxhat - mean(dxhat) - xhat * mean(dxhat * xhat)),
 // dxhat = dout * gamma.  One wave per row; the row stays in registers.
 template <typename T, int CH>
-__global__ void __launch_bounds__(256) ln_bwd_kernel(int rows, int h, const T* __restrict__ dout,
+__global__ void __launch_bounds__(256) ln_bwd_kernel(int rows, int mrows, int mstride, int h,
+                                                     const T* __restrict__ dout,
                                                      const T* __restrict__ x, const float* __restrict__ mean,
                                                      const float* __restrict__ rstd, const T* __restrict__ gamma,
                                                      const T* __restrict__ dres, T* __restrict__ dx) {
-  const int row = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+  const int lrow = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  if (row >= rows) return;
+  if (lrow >= rows) return;
+  const int row = member_row(lrow, mrows, mstride);
   const float mu = mean[row], rs = rstd[row];
   const T* xr = x + (size_t)row * h;
   const T* dr = dout + (size_t)row * h;
@@ -208,67 +219,83 @@ __global__ void __launch_bounds__(64 * kReduceWaves) reduce_partials_kernel(int 
 // ---------------------------------------------------------------------------
 // Host launchers
 // ---------------------------------------------------------------------------
+// Rows of one launch: `rows` logical rows in groups of mrows, mstride apart.
+struct RowMap {
+  int rows, mrows, mstride;
+};
+
 template <typename T, int CH>
-static hipError_t ln_fwd_t(int rows, int h, float eps, const void* x, const void* g, const void* b, void* y,
+static hipError_t ln_fwd_t(RowMap rm, int h, float eps, const void* x, const void* g, const void* b, void* y,
                            float* mean, float* rstd, hipStream_t s) {
-  dim3 grid((rows + kRowsPerBlock - 1) / kRowsPerBlock);
-  hipLaunchKernelGGL((ln_fwd_kernel<T, CH>), grid, dim3(256), 0, s, rows, h, eps, (const T*)x, (const T*)g,
-                     (const T*)b, (T*)y, mean, rstd);
+  dim3 grid((rm.rows + kRowsPerBlock - 1) / kRowsPerBlock);
+  hipLaunchKernelGGL((ln_fwd_kernel<T, CH>), grid, dim3(256), 0, s, rm.rows, rm.mrows, rm.mstride, h, eps,
+                     (const T*)x, (const T*)g, (const T*)b, (T*)y, mean, rstd);
   return hipGetLastError();
 }
 
 template <typename T>
-static hipError_t ln_fwd_dispatch(int rows, int h, float eps, const void* x, const void* g, const void* b,
+static hipError_t ln_fwd_dispatch(RowMap rm, int h, float eps, const void* x, const void* g, const void* b,
                                   void* y, float* mean, float* rstd, hipStream_t s) {
   const int ch = (h + 511) / 512;
-  if (ch <= 1) return ln_fwd_t<T, 1>(rows, h, eps, x, g, b, y, mean, rstd, s);
-  if (ch <= 2) return ln_fwd_t<T, 2>(rows, h, eps, x, g, b, y, mean, rstd, s);
-  if (ch <= 4) return ln_fwd_t<T, 4>(rows, h, eps, x, g, b, y, mean, rstd, s);
-  if (ch <= 6) return ln_fwd_t<T, 6>(rows, h, eps, x, g, b, y, mean, rstd, s);
-  if (ch <= 8) return ln_fwd_t<T, 8>(rows, h, eps, x, g, b, y, mean, rstd, s);
-  if (ch <= 12) return ln_fwd_t<T, 12>(rows, h, eps, x, g, b, y, mean, rstd, s);
-  if (ch <= 16) return ln_fwd_t<T, 16>(rows, h, eps, x, g, b, y, mean, rstd, s);
+  if (ch <= 1) return ln_fwd_t<T, 1>(rm, h, eps, x, g, b, y, mean, rstd, s);
+  if (ch <= 2) return ln_fwd_t<T, 2>(rm, h, eps, x, g, b, y, mean, rstd, s);
+  if (ch <= 4) return ln_fwd_t<T, 4>(rm, h, eps, x, g, b, y, mean, rstd, s);
+  if (ch <= 6) return ln_fwd_t<T, 6>(rm, h, eps, x, g, b, y, mean, rstd, s);
+  if (ch <= 8) return ln_fwd_t<T, 8>(rm, h, eps, x, g, b, y, mean, rstd, s);
+  if (ch <= 12) return ln_fwd_t<T, 12>(rm, h, eps, x, g, b, y, mean, rstd, s);
+  if (ch <= 16) return ln_fwd_t<T, 16>(rm, h, eps, x, g, b, y, mean, rstd, s);
   return hipErrorInvalidValue;
 }
 
+static bool row_map(int rows, int members, int member_stride, RowMap* rm) {
+  if (members < 1 || (members > 1 && member_stride < rows)) return false;
+  if ((long long)rows * members > 0x7fffffffLL || (long long)member_stride * (members - 1) + rows > 0x7fffffffLL)
+    return false;
+  *rm = {rows * members, rows, members > 1 ? member_stride : rows};
+  return true;
+}
+
 hipError_t launch_layernorm_fwd(int dtype, int rows, int h, float eps, const void* x, const void* gamma,
-                                const void* beta, void* y, float* mean, float* rstd, hipStream_t stream) {
+                                const void* beta, void* y, float* mean, float* rstd, hipStream_t stream,
+                                int members, int member_stride) {
   if (rows <= 0) return hipSuccess;
-  if (h % 8 != 0) return hipErrorInvalidValue;
-  return dtype == DT_BF16 ? ln_fwd_dispatch<bf16_t>(rows, h, eps, x, gamma, beta, y, mean, rstd, stream)
-                          : ln_fwd_dispatch<float>(rows, h, eps, x, gamma, beta, y, mean, rstd, stream);
+  RowMap rm;
+  if (h % 8 != 0 || !row_map(rows, members, member_stride, &rm)) return hipErrorInvalidValue;
+  return dtype == DT_BF16 ? ln_fwd_dispatch<bf16_t>(rm, h, eps, x, gamma, beta, y, mean, rstd, stream)
+                          : ln_fwd_dispatch<float>(rm, h, eps, x, gamma, beta, y, mean, rstd, stream);
 }
 
 template <typename T, int CH>
-static hipError_t ln_bwd_t(int rows, int h, const void* dout, const void* x, const float* mean,
+static hipError_t ln_bwd_t(RowMap rm, int h, const void* dout, const void* x, const float* mean,
                            const float* rstd, const void* g, const void* dres, void* dx, hipStream_t s) {
-  dim3 grid((rows + kRowsPerBlock - 1) / kRowsPerBlock);
-  hipLaunchKernelGGL((ln_bwd_kernel<T, CH>), grid, dim3(256), 0, s, rows, h, (const T*)dout, (const T*)x, mean,
-                     rstd, (const T*)g, (const T*)dres, (T*)dx);
+  dim3 grid((rm.rows + kRowsPerBlock - 1) / kRowsPerBlock);
+  hipLaunchKernelGGL((ln_bwd_kernel<T, CH>), grid, dim3(256), 0, s, rm.rows, rm.mrows, rm.mstride, h,
+                     (const T*)dout, (const T*)x, mean, rstd, (const T*)g, (const T*)dres, (T*)dx);
   return hipGetLastError();
 }
 
 template <typename T>
-static hipError_t ln_bwd_dispatch(int rows, int h, const void* dout, const void* x, const float* mean,
+static hipError_t ln_bwd_dispatch(RowMap rm, int h, const void* dout, const void* x, const float* mean,
                                   const float* rstd, const void* g, const void* dres, void* dx, hipStream_t s) {
   const int ch = (h + 511) / 512;
-  if (ch <= 1) return ln_bwd_t<T, 1>(rows, h, dout, x, mean, rstd, g, dres, dx, s);
-  if (ch <= 2) return ln_bwd_t<T, 2>(rows, h, dout, x, mean, rstd, g, dres, dx, s);
-  if (ch <= 4) return ln_bwd_t<T, 4>(rows, h, dout, x, mean, rstd, g, dres, dx, s);
-  if (ch <= 6) return ln_bwd_t<T, 6>(rows, h, dout, x, mean, rstd, g, dres, dx, s);
-  if (ch <= 8) return ln_bwd_t<T, 8>(rows, h, dout, x, mean, rstd, g, dres, dx, s);
-  if (ch <= 12) return ln_bwd_t<T, 12>(rows, h, dout, x, mean, rstd, g, dres, dx, s);
-  if (ch <= 16) return ln_bwd_t<T, 16>(rows, h, dout, x, mean, rstd, g, dres, dx, s);
+  if (ch <= 1) return ln_bwd_t<T, 1>(rm, h, dout, x, mean, rstd, g, dres, dx, s);
+  if (ch <= 2) return ln_bwd_t<T, 2>(rm, h, dout, x, mean, rstd, g, dres, dx, s);
+  if (ch <= 4) return ln_bwd_t<T, 4>(rm, h, dout, x, mean, rstd, g, dres, dx, s);
+  if (ch <= 6) return ln_bwd_t<T, 6>(rm, h, dout, x, mean, rstd, g, dres, dx, s);
+  if (ch <= 8) return ln_bwd_t<T, 8>(rm, h, dout, x, mean, rstd, g, dres, dx, s);
+  if (ch <= 12) return ln_bwd_t<T, 12>(rm, h, dout, x, mean, rstd, g, dres, dx, s);
+  if (ch <= 16) return ln_bwd_t<T, 16>(rm, h, dout, x, mean, rstd, g, dres, dx, s);
   return hipErrorInvalidValue;
 }
 
 hipError_t launch_layernorm_bwd(int dtype, int rows, int h, const void* dout, const void* x, const float* mean,
                                 const float* rstd, const void* gamma, const void* dres, void* dx,
-                                hipStream_t stream) {
+                                hipStream_t stream, int members, int member_stride) {
   if (rows <= 0) return hipSuccess;
-  if (h % 8 != 0) return hipErrorInvalidValue;
-  return dtype == DT_BF16 ? ln_bwd_dispatch<bf16_t>(rows, h, dout, x, mean, rstd, gamma, dres, dx, stream)
-                          : ln_bwd_dispatch<float>(rows, h, dout, x, mean, rstd, gamma, dres, dx, stream);
+  RowMap rm;
+  if (h % 8 != 0 || !row_map(rows, members, member_stride, &rm)) return hipErrorInvalidValue;
+  return dtype == DT_BF16 ? ln_bwd_dispatch<bf16_t>(rm, h, dout, x, mean, rstd, gamma, dres, dx, stream)
+                          : ln_bwd_dispatch<float>(rm, h, dout, x, mean, rstd, gamma, dres, dx, stream);
 }
 
 template <int MODE>
@@ -302,54 +329,6 @@ hipError_t launch_reduce_partials(int groups, int cols, const float* part, float
   dim3 grid((cols + 63) / 64);
   hipLaunchKernelGGL(reduce_partials_kernel, grid, dim3(64 * kReduceWaves), 0, stream, groups, cols, part, out,
                      accumulate);
-  return hipGetLastError();
-}
-
-// ---------------------------------------------------------------------------
-// Transpose dst[c, r] = src[r, c] of a [rows, cols] matrix (rows, cols
-// multiples of 64; leading dimensions in elements).  One 64 x 64 tile per
-// workgroup through LDS: rows are read and written as contiguous 16-byte
-// (bf16) or 16-byte x 2 (fp32) chunks.
-// ---------------------------------------------------------------------------
-template <typename T>
-__global__ void __launch_bounds__(256) transpose_kernel(int rows, int cols, const T* __restrict__ src, int lds_,
-                                                        T* __restrict__ dst, int ldd) {
-  __shared__ T tile[64][64 + 8 / sizeof(T) * 2];
-  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
-  const int tid = threadIdx.x;
-  // 64 rows x 8 chunks of 8 elements
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int idx = tid + i * 256;
-    const int r = idx >> 3, ch = idx & 7;
-    float v[8];
-    load8(src + (size_t)(r0 + r) * lds_ + c0 + ch * 8, v);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) tile[r][ch * 8 + e] = Elem<T>::from_f(v[e]);
-  }
-  __syncthreads();
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int idx = tid + i * 256;
-    const int c = idx >> 3, ch = idx & 7;  // output row c (= input column), 8 input rows
-    float v[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) v[e] = Elem<T>::to_f(tile[ch * 8 + e][c]);
-    store8(dst + (size_t)(c0 + c) * ldd + r0 + ch * 8, v);
-  }
-}
-
-hipError_t launch_transpose(int dtype, int rows, int cols, const void* src, int ld_src, void* dst, int ld_dst,
-                            hipStream_t stream) {
-  if (rows <= 0 || cols <= 0) return hipSuccess;
-  if (rows % 64 || cols % 64) return hipErrorInvalidValue;
-  dim3 grid(cols / 64, rows / 64);
-  if (dtype == DT_BF16)
-    hipLaunchKernelGGL((transpose_kernel<bf16_t>), grid, dim3(256), 0, stream, rows, cols, (const bf16_t*)src, ld_src,
-                       (bf16_t*)dst, ld_dst);
-  else
-    hipLaunchKernelGGL((transpose_kernel<float>), grid, dim3(256), 0, stream, rows, cols, (const float*)src, ld_src,
-                       (float*)dst, ld_dst);
   return hipGetLastError();
 }
 

@@ -166,9 +166,6 @@ struct WsLayout {
   size_t chain;       // 3 input-gradient buffers
   size_t par[2];      // backward scratch per parity
   size_t rc_y;        // recompute's (unused) block output
-  size_t wt;          // transposed weights of every block (backward input gradients)
-  size_t wt_off[4];   // per block: W_qkv^T [h][3h/t], W_o^T [h/t][h], W1^T [h][f/t], W2^T [f/t][h] (bytes)
-  size_t wt_stride;   // bytes per block
   size_t total;
   size_t recompute_total;
   int keep_slot[kMaxBlocks];  // index among kept blocks, or -1
@@ -195,16 +192,6 @@ WsLayout ws_layout(const Dims& D) {
   W.par[0] = o; o += W.bwd.size;
   W.par[1] = o; o += W.bwd.size;
   W.rc_y = o; o += (W.n_rc > 0 ? th : 0);
-  {
-    const size_t sizes[4] = {(size_t)3 * D.hl * D.h, (size_t)D.h * D.hl, (size_t)D.fl * D.h, (size_t)D.h * D.fl};
-    size_t b = 0;
-    for (int i = 0; i < 4; ++i) {
-      W.wt_off[i] = b;
-      b = align_up(b + sizes[i] * D.esz, 256);
-    }
-    W.wt_stride = b;
-  }
-  W.wt = o; o += (size_t)D.L * W.wt_stride;
   W.total = o;
   W.recompute_total = (size_t)W.n_rc * W.act.size;
   return W;
@@ -227,7 +214,6 @@ struct merak_stage {
   char* rc;
   hipStream_t aux;
   hipEvent_t ev_fork, ev_s1, ev_j0, ev_j1, ev_aux, ev_dw[2];
-  hipEvent_t ev_wt[kMaxBlocks];  // transposed weights of block l ready
   hipEvent_t ev_rc[kMaxBlocks][2];  // recompute of block l done on its two streams
   int state;  // 0 idle, 1 forward pending, 2 recomputed
   const void* x0;
@@ -292,24 +278,6 @@ inline const char* P(const void* params, const merak_stage* S, int l, int which)
   return (const char*)params + (S->p_stride * l + S->p_off[which]) * S->D.esz;
 }
 
-// Transposed weight i of block l (0 W_qkv^T, 1 W_o^T, 2 W1^T, 3 W2^T): the
-// weight stored [in][out], so the input-gradient GEMMs read both operands
-// along K.
-inline const char* WT(const merak_stage* S, int l, int i) {
-  return S->ws + S->W.wt + (size_t)l * S->W.wt_stride + S->W.wt_off[i];
-}
-
-// Fill the transposed weights of block l.
-int transpose_weights(merak_stage* S, const void* params, int l, hipStream_t st) {
-  const Dims& D = S->D;
-  struct T { int which, rows, cols, dst; };
-  const T t[4] = {{P_WQKV, 3 * D.hl, D.h, 0}, {P_WO, D.h, D.hl, 1}, {P_W1, D.fl, D.h, 2}, {P_W2, D.h, D.fl, 3}};
-  for (const T& x : t)
-    LAUNCH(MERAK_KC_TRANSPOSE, st, launch_transpose(D.dtype, x.rows, x.cols, P(params, S, l, x.which), x.cols,
-                                                    (void*)WT(S, l, x.dst), x.rows, st));
-  return MERAK_OK;
-}
-
 GemmProblem gp(int M, int N, int K, const void* a, int lda, const void* b, int ldb, void* c, int ldc,
                const void* bias = nullptr, const void* resid = nullptr, void* aux = nullptr, int acc = 0) {
   GemmProblem p;
@@ -322,8 +290,8 @@ GemmProblem gp(int M, int N, int K, const void* a, int lda, const void* b, int l
 //   0 LN1  1 QKV GEMM  2 attention  3 projection GEMM  4 LN2  5 FC1 GEMM
 //   6 FC2 GEMM.
 // GEMM steps only describe their problem (*p, *epi) for a grouped launch; the
-// other steps are launched on st.  The attention step covers `members`
-// sub-micro-batches j, j + 2, ... in one launch.
+// other steps are launched on st, each covering `members` sub-micro-batches
+// j, j + 2, ... in one launch.
 constexpr int kFwdSteps = 7;
 inline bool fwd_step_is_gemm(int k) { return k == 1 || k == 3 || k == 5 || k == 6; }
 int block_forward_step(merak_stage* S, const void* params, int l, int j, int k, char* A, const char* x, char* y,
@@ -338,7 +306,7 @@ int block_forward_step(merak_stage* S, const void* params, int l, int j, int k, 
     case 0:  // LN1
       LAUNCH(MERAK_KC_LN_FWD, st, launch_layernorm_fwd(dt, M, D.h, D.eps, x + r0 * D.h * e, P(params, S, l, P_LN1G),
                                    P(params, S, l, P_LN1B), A + L.ln1 + r0 * D.h * e, (float*)(A + L.mu1) + r0,
-                                   (float*)(A + L.rs1) + r0, st));
+                                   (float*)(A + L.rs1) + r0, st, members, 2 * M));
       break;
     case 1:  // QKV (column parallel) + bias
       *p = gp(M, 3 * D.hl, D.h, A + L.ln1 + r0 * D.h * e, D.h, P(params, S, l, P_WQKV), D.h,
@@ -359,7 +327,7 @@ int block_forward_step(merak_stage* S, const void* params, int l, int j, int k, 
     case 4:  // LN2
       LAUNCH(MERAK_KC_LN_FWD, st, launch_layernorm_fwd(dt, M, D.h, D.eps, A + L.x1 + r0 * D.h * e,
                                    P(params, S, l, P_LN2G), P(params, S, l, P_LN2B), A + L.ln2 + r0 * D.h * e,
-                                   (float*)(A + L.mu2) + r0, (float*)(A + L.rs2) + r0, st));
+                                   (float*)(A + L.mu2) + r0, (float*)(A + L.rs2) + r0, st, members, 2 * M));
       break;
     case 5:  // FC1 (column parallel) + bias + GeLU; keeps the pre-activation u
       *p = gp(M, D.fl, D.h, A + L.ln2 + r0 * D.h * e, D.h, P(params, S, l, P_W1), D.h, A + L.g + r0 * D.fl * e, D.fl,
@@ -389,7 +357,7 @@ int block_forward(merak_stage* S, const void* params, int l, char* A, const char
       int np = 0, epi = EPI_STORE;
       const int members = (D.n - par + 1) / 2;  // sub-micro-batches on this stream
       for (int j = par; j < D.n; j += 2) {
-        if (k == 2 && j != par) break;  // one attention launch covers the stream's sub-micro-batches
+        if (!fwd_step_is_gemm(k) && j != par) break;  // one LN / attention launch covers them all
         TRY_INNER(block_forward_step(S, params, l, j, k, A, x, y, part_o, part_f, st, &probs[np], &epi, members));
         if (fwd_step_is_gemm(k) && (++np == kMaxGroup || j + 2 >= D.n)) {
           LAUNCH(MERAK_KC_GEMM_FWD, st, launch_gemm(D.dtype, false, false, epi, probs, np, st));
@@ -404,8 +372,9 @@ int block_forward(merak_stage* S, const void* params, int l, char* A, const char
 // Step k (0..6) of the input-gradient chain of block l for sub-micro-batch j:
 //   0 FC2 dX (+GeLU')  1 FC1 dX  2 LN2 bwd  3 proj dX  4 attention bwd
 //   5 QKV dX  6 LN1 bwd.
-// GEMM steps only describe their problem for a grouped launch; the attention
-// step covers `members` sub-micro-batches j, j + 2, ... in one launch.
+// GEMM steps only describe their problem for a grouped launch; the LayerNorm
+// and attention steps cover `members` sub-micro-batches j, j + 2, ... in one
+// launch.
 constexpr int kChainSteps = 7;
 inline bool bwd_step_is_gemm(int k) { return k == 0 || k == 1 || k == 3 || k == 5; }
 int block_backward_step(merak_stage* S, const void* params, int l, int j, int k, const char* A, const char* x,
@@ -420,21 +389,22 @@ int block_backward_step(merak_stage* S, const void* params, int l, int j, int k,
   const int M = D.Ms;
   switch (k) {
     case 0:  // FC2 backward: dg = dy W2; du = dg * gelu'(u)
-      *gpr = gp(M, D.fl, D.h, dy + r0 * D.h * e, D.h, WT(S, l, 3), D.h, B + Bl.du + r0 * D.fl * e, D.fl, nullptr,
+      *gpr = gp(M, D.fl, D.h, dy + r0 * D.h * e, D.h, P(params, S, l, P_W2), D.fl, B + Bl.du + r0 * D.fl * e, D.fl, nullptr,
                 nullptr, (void*)(A + L.u + r0 * D.fl * e));
       *epi = EPI_GELU_BWD;
       break;
     case 1:  // FC1 backward: d_ln2 partial = du W1 (hand-off)
-      *gpr = gp(M, D.h, D.fl, B + Bl.du + r0 * D.fl * e, D.fl, WT(S, l, 2), D.fl, d_ln2 + r0 * D.h * e, D.h);
+      *gpr = gp(M, D.h, D.fl, B + Bl.du + r0 * D.fl * e, D.fl, P(params, S, l, P_W1), D.h, d_ln2 + r0 * D.h * e, D.h);
       *epi = EPI_STORE;
       break;
     case 2:  // LN2 backward + residual gradient: dx1 = dy + LN2'(d_ln2)
       LAUNCH(MERAK_KC_LN_BWD, st, launch_layernorm_bwd(dt, M, D.h, d_ln2 + r0 * D.h * e, A + L.x1 + r0 * D.h * e,
                                  (const float*)(A + L.mu2) + r0, (const float*)(A + L.rs2) + r0,
-                                 P(params, S, l, P_LN2G), dy + r0 * D.h * e, B + Bl.dx1 + r0 * D.h * e, st));
+                                 P(params, S, l, P_LN2G), dy + r0 * D.h * e, B + Bl.dx1 + r0 * D.h * e, st,
+                                 members, 2 * M));
       break;
     case 3:  // projection backward: dO = dx1 W_o
-      *gpr = gp(M, D.hl, D.h, B + Bl.dx1 + r0 * D.h * e, D.h, WT(S, l, 1), D.h, B + Bl.dO + r0 * D.hl * e, D.hl);
+      *gpr = gp(M, D.hl, D.h, B + Bl.dx1 + r0 * D.h * e, D.h, P(params, S, l, P_WO), D.hl, B + Bl.dO + r0 * D.hl * e, D.hl);
       *epi = EPI_STORE;
       break;
     case 4: {  // attention backward -> dqkv
@@ -446,14 +416,15 @@ int block_backward_step(merak_stage* S, const void* params, int l, int j, int k,
       break;
     }
     case 5:  // QKV backward: d_ln1 partial = dqkv W_qkv (hand-off)
-      *gpr = gp(M, D.h, 3 * D.hl, B + Bl.dqkv + r0 * 3 * D.hl * e, 3 * D.hl, WT(S, l, 0), 3 * D.hl,
+      *gpr = gp(M, D.h, 3 * D.hl, B + Bl.dqkv + r0 * 3 * D.hl * e, 3 * D.hl, P(params, S, l, P_WQKV), D.h,
                 d_ln1 + r0 * D.h * e, D.h);
       *epi = EPI_STORE;
       break;
     default:  // LN1 backward + residual gradient: dx = dx1 + LN1'(d_ln1)
       LAUNCH(MERAK_KC_LN_BWD, st, launch_layernorm_bwd(dt, M, D.h, d_ln1 + r0 * D.h * e, x + r0 * D.h * e,
                                  (const float*)(A + L.mu1) + r0, (const float*)(A + L.rs1) + r0,
-                                 P(params, S, l, P_LN1G), B + Bl.dx1 + r0 * D.h * e, dx + r0 * D.h * e, st));
+                                 P(params, S, l, P_LN1G), B + Bl.dx1 + r0 * D.h * e, dx + r0 * D.h * e, st,
+                                 members, 2 * M));
       break;
   }
   return MERAK_OK;
@@ -462,9 +433,12 @@ int block_backward_step(merak_stage* S, const void* params, int l, int j, int k,
 // Weight, bias and LayerNorm gradients of block l over the whole micro-batch,
 // in two groups: group 0 (W2, b2, W1, b1) needs only dy and du, i.e. the FC2
 // backward of every sub-micro-batch; group 1 (W_o, b_o, W_qkv, b_qkv and both
-// LayerNorms) needs the rest of the chain.
+// LayerNorms) needs the rest of the chain.  The GEMMs go on st; group 1's
+// bias reductions on st_b and its LayerNorm reductions on st_ln (all three may
+// be the same stream; each must already follow the whole chain).
 int block_param_grads(merak_stage* S, int l, int group, const char* A, const char* x, const char* dy, const char* B,
-                      const char* d_ln1, const char* d_ln2, float* grads, int acc, hipStream_t st) {
+                      const char* d_ln1, const char* d_ln2, float* grads, int acc, hipStream_t st,
+                      hipStream_t st_b = nullptr, hipStream_t st_ln = nullptr) {
   const Dims& D = S->D;
   const ActLayout& L = S->W.act;
   const BwdLayout& Bl = S->W.bwd;
@@ -493,6 +467,9 @@ int block_param_grads(merak_stage* S, int l, int group, const char* A, const cha
             nullptr, acc);
   p[1] = gp(D.h, D.hl, T, B + Bl.dx1, D.h, A + L.o, D.hl, g + S->p_off[P_WO], D.hl, nullptr, nullptr, nullptr, acc);
   LAUNCH(MERAK_KC_GEMM_DW_ATTN, st, launch_gemm(dt, true, true, EPI_F32, p, 2, st));
+  if (!st_b) st_b = st;
+  if (!st_ln) st_ln = st;
+  st = st_b;
   pb = (float*)(B + Bl.p_bqkv);
   LAUNCH(MERAK_KC_REDUCE, st, launch_column_partials(dt, T, 3 * D.hl, B + Bl.dqkv, pb, st));
   LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials(G, 3 * D.hl, pb, g + S->p_off[P_BQKV], acc, st));
@@ -500,6 +477,7 @@ int block_param_grads(merak_stage* S, int l, int group, const char* A, const cha
   LAUNCH(MERAK_KC_REDUCE, st, launch_column_partials(dt, T, D.h, B + Bl.dx1, pb, st));
   LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials(G, D.h, pb, g + S->p_off[P_BO], acc, st));
   // LayerNorm parameters
+  st = st_ln;
   float* pg = (float*)(B + Bl.p_g2);
   float* pbe = (float*)(B + Bl.p_be2);
   LAUNCH(MERAK_KC_REDUCE, st, launch_layernorm_param_partials(dt, T, D.h, d_ln2, A + L.x1, (const float*)(A + L.mu2),
@@ -620,11 +598,7 @@ int merak_stage_create(const merak_stage_config* cfg, void* workspace, size_t wo
     e = hipEventCreateWithFlags(ev, hipEventDisableTiming);
     if (e == hipSuccess) ++made;
   }
-  int made_wt = 0, made_rc = 0;
-  for (int l = 0; l < D.L && e == hipSuccess; ++l) {
-    e = hipEventCreateWithFlags(&S->ev_wt[l], hipEventDisableTiming);
-    if (e == hipSuccess) ++made_wt;
-  }
+  int made_rc = 0;
   for (int l = 0; l < D.L && e == hipSuccess; ++l) {
     e = hipEventCreateWithFlags(&S->ev_rc[l][0], hipEventDisableTiming);
     if (e != hipSuccess) break;
@@ -637,7 +611,6 @@ int merak_stage_create(const merak_stage_config* cfg, void* workspace, size_t wo
   }
   if (e != hipSuccess) {
     for (int i = 0; i < made; ++i) (void)hipEventDestroy(*evs[i]);
-    for (int l = 0; l < made_wt; ++l) (void)hipEventDestroy(S->ev_wt[l]);
     for (int l = 0; l < made_rc; ++l) {
       (void)hipEventDestroy(S->ev_rc[l][0]);
       (void)hipEventDestroy(S->ev_rc[l][1]);
@@ -660,7 +633,6 @@ int merak_stage_destroy(merak_stage_t S) {
   hipEvent_t evs[] = {S->ev_fork, S->ev_s1, S->ev_j0, S->ev_j1, S->ev_aux, S->ev_dw[0], S->ev_dw[1]};
   for (hipEvent_t ev : evs) (void)hipEventDestroy(ev);
   for (int l = 0; l < S->D.L; ++l) {
-    (void)hipEventDestroy(S->ev_wt[l]);
     (void)hipEventDestroy(S->ev_rc[l][0]);
     (void)hipEventDestroy(S->ev_rc[l][1]);
   }
@@ -778,12 +750,6 @@ int merak_stage_bwd(merak_stage_t S, const void* params, const void* dy, void* d
   const size_t th_al = align_up(th, 256);
   TRY(fork(S, s0, s1));
   HIP_TRY(hipStreamWaitEvent(S->aux, S->ev_fork, 0));
-  // Transposed weights for the input-gradient GEMMs, made from this call's
-  // parameters on the internal stream, last block first.
-  for (int l = D.L - 1; l >= 0; --l) {
-    TRY(transpose_weights(S, params, l, S->aux));
-    HIP_TRY(hipEventRecord(S->ev_wt[l], S->aux));
-  }
   for (int l = D.L - 1; l >= 0; --l) {
     const int par = l & 1;
     char* A = block_acts(S, l, 1);
@@ -797,8 +763,6 @@ int merak_stage_bwd(merak_stage_t S, const void* params, const void* dy, void* d
       HIP_TRY(hipStreamWaitEvent(s0, S->ev_dw[par], 0));
       HIP_TRY(hipStreamWaitEvent(s1, S->ev_dw[par], 0));
     }
-    HIP_TRY(hipStreamWaitEvent(s0, S->ev_wt[l], 0));
-    HIP_TRY(hipStreamWaitEvent(s1, S->ev_wt[l], 0));
     if ((D.mask >> l) & 1) {  // the activations recomputed for this block
       for (int q = 0; q < 2; ++q) {
         HIP_TRY(hipStreamWaitEvent(s0, S->ev_rc[l][q], 0));
@@ -817,10 +781,10 @@ int merak_stage_bwd(merak_stage_t S, const void* params, const void* dy, void* d
         int np = 0, epi = EPI_STORE;
         const int members = (D.n - sp + 1) / 2;  // sub-micro-batches on this stream
         for (int j = sp; j < D.n; j += 2) {
-          if (k == 4 && j != sp) break;  // one attention launch covers the stream's sub-micro-batches
+          if (!bwd_step_is_gemm(k) && j != sp) break;  // one LN / attention launch covers them all
           TRY(block_backward_step(S, params, l, j, k, A, xin, dyl, dxl, B, d1, d2, st, &probs[np], &epi, members));
           if (bwd_step_is_gemm(k) && (++np == kMaxGroup || j + 2 >= D.n)) {
-            LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(D.dtype, false, false, epi, probs, np, st));
+            LAUNCH(MERAK_KC_GEMM_DX, st, launch_gemm(D.dtype, false, true, epi, probs, np, st));
             np = 0;
           }
         }
@@ -830,7 +794,16 @@ int merak_stage_bwd(merak_stage_t S, const void* params, const void* dy, void* d
         HIP_TRY(hipEventRecord(S->ev_j1, s1));
         HIP_TRY(hipStreamWaitEvent(S->aux, S->ev_j0, 0));
         HIP_TRY(hipStreamWaitEvent(S->aux, S->ev_j1, 0));
-        TRY(block_param_grads(S, l, k == 0 ? 0 : 1, A, xin, dyl, B, d1, d2, grads, accumulate, S->aux));
+        if (k == 0 || l > 0) {
+          TRY(block_param_grads(S, l, k == 0 ? 0 : 1, A, xin, dyl, B, d1, d2, grads, accumulate, S->aux));
+        } else {
+          // Last block: the chains are done, so s0 and s1 take the bias and
+          // LayerNorm reductions beside the weight-gradient GEMM instead of
+          // queueing them after it on the internal stream.
+          HIP_TRY(hipStreamWaitEvent(s0, S->ev_j1, 0));
+          HIP_TRY(hipStreamWaitEvent(s1, S->ev_j0, 0));
+          TRY(block_param_grads(S, l, 1, A, xin, dyl, B, d1, d2, grads, accumulate, S->aux, s0, s1));
+        }
       }
     }
     HIP_TRY(hipEventRecord(S->ev_dw[par], S->aux));
