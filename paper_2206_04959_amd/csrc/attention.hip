@@ -145,8 +145,10 @@ __global__ void __launch_bounds__(256) attn_fwd_bf16(int S, int H, int Bm, int m
   constexpr int LD = TT::LD, KS = D / 16, DT = D / 32, TB = TT::BYTES;
   extern __shared__ __align__(16) char smem[];  // [stage][K blk a, K blk b, V blk a, V blk b]
 
-  const int b = seq_index(blockIdx.z, Bm, mstride), hh = blockIdx.y;
-  const int qt = gridDim.x - 1 - blockIdx.x;  // longest rows first
+  // Grid (heads, sequences, row blocks), row block slowest: the whole grid
+  // runs longest rows first.
+  const int b = seq_index(blockIdx.y, Bm, mstride), hh = blockIdx.x;
+  const int qt = gridDim.z - 1 - blockIdx.z;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, l32 = lane & 31, hf = lane >> 5;
   const int qg = wave & 1, kh = wave >> 1;
   const int q0 = qt * 64 + qg * 32;
@@ -337,8 +339,10 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_bf16(int S, int H, int Bm, 
   extern __shared__ __align__(16) char smem[];  // [stage][Q a, Q b, dO a, dO b], then lse/delta
   float* vecs = reinterpret_cast<float*>(smem + kAttnStages * 4 * TB);  // [stage][lse a|b, delta a|b]
 
-  const int b = seq_index(blockIdx.z, Bm, mstride), hh = blockIdx.y;
-  const int kt = blockIdx.x;  // early keys see the most queries: dispatched first
+  // Grid (heads, sequences, key blocks), key block slowest: early keys see the
+  // most queries, so the whole grid runs longest columns first.
+  const int b = seq_index(blockIdx.y, Bm, mstride), hh = blockIdx.x;
+  const int kt = blockIdx.z;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, l32 = lane & 31, hf = lane >> 5;
   const int kg = wave & 1, qh = wave >> 1;
   const int kw0 = kt * 64 + kg * 32;
@@ -488,8 +492,8 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_bf16(int S, int H, int Bm, in
   constexpr int LD = TT::LD, KS = D / 16, DT = D / 32, TB = TT::BYTES;
   extern __shared__ __align__(16) char smem[];
 
-  const int b = seq_index(blockIdx.z, Bm, mstride), hh = blockIdx.y;
-  const int qt = gridDim.x - 1 - blockIdx.x;
+  const int b = seq_index(blockIdx.y, Bm, mstride), hh = blockIdx.x;  // grid as in the forward
+  const int qt = gridDim.z - 1 - blockIdx.z;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, l32 = lane & 31, hf = lane >> 5;
   const int qg = wave & 1, kh = wave >> 1;
   const int q0 = qt * 64 + qg * 32;
@@ -749,7 +753,7 @@ static hipError_t fwd_d(int dtype, int B, int S, int H, int G, int mstride, cons
     static bool ok = false;
     hipError_t e = allow_lds(attn_fwd_bf16<D>, lds, ok);
     if (e != hipSuccess) return e;
-    dim3 grid(S / 64, H, G * B);
+    dim3 grid(H, G * B, S / 64);
     hipLaunchKernelGGL((attn_fwd_bf16<D>), grid, dim3(256), lds, st, S, H, B, mstride, (const bf16_t*)qkv,
                        (bf16_t*)o, lse, scale * kLog2e);
   } else {
@@ -779,7 +783,7 @@ static hipError_t bwd_d(int dtype, int B, int S, int H, int G, int mstride, cons
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((attn_delta_kernel<bf16_t, D>), dim3((rows + 255) / 256), dim3(256), 0, st, G * B, S, H, B,
                        mstride, (const bf16_t*)o, (const bf16_t*)dout, delta);
-    dim3 grid(S / 64, H, G * B);
+    dim3 grid(H, G * B, S / 64);
     hipLaunchKernelGGL((attn_bwd_dkdv_bf16<D>), grid, dim3(256), lds_k, st, S, H, B, mstride, (const bf16_t*)qkv,
                        (const bf16_t*)dout, lse, delta, (bf16_t*)dqkv, scale * kLog2e, scale);
     hipLaunchKernelGGL((attn_bwd_dq_bf16<D>), grid, dim3(256), lds_q, st, S, H, B, mstride, (const bf16_t*)qkv,
