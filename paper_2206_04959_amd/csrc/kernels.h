@@ -69,6 +69,28 @@ hipError_t launch_column_partials(int dtype, int rows, int cols, const void* x, 
 hipError_t launch_reduce_partials(int groups, int cols, const float* part, float* out, int accumulate,
                                   hipStream_t stream);
 
+// Batched forms: up to kMaxColJobs independent reductions in one launch, with
+// the same per-job results as the single calls above.
+constexpr int kMaxColJobs = 6;
+struct ColPartialJob {
+  int mode;  // 0: p0 = column partials of a; 1: LayerNorm parameter partials (a = dout)
+  int rows, cols;
+  const void* a;
+  const void* x;  // mode 1: LayerNorm input, with mean and rstd
+  const float* mean;
+  const float* rstd;
+  float* p0;
+  float* p1;  // mode 1: partials of sum dout
+};
+hipError_t launch_column_partials_batch(int dtype, const ColPartialJob* jobs, int n, hipStream_t stream);
+struct ReduceJob {
+  int groups, cols;
+  const float* part;
+  float* out;
+  int accumulate;
+};
+hipError_t launch_reduce_partials_batch(const ReduceJob* jobs, int n, hipStream_t stream);
+
 // Causal attention on packed qkv [batch, seq, 3, heads, d].  One launch may
 // cover `members` groups of `batch` sequences each, member m starting
 // m * member_stride sequences after the pointers given (so the sub-micro-

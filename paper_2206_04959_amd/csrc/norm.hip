@@ -131,40 +131,43 @@ __global__ void __launch_bounds__(256) ln_bwd_kernel(int rows, int mrows, int ms
   }
 }
 
-// Segment/slice partial sums.  MODE 0: part0 = sum x.  MODE 1 (LayerNorm
-// parameters): part0 = sum dout * xhat, part1 = sum dout, with xhat rebuilt from
-// x, mean and rstd.
+// Segment/slice partial sums.  Mode 0: part0 = sum a.  Mode 1 (LayerNorm
+// parameters): part0 = sum a * xhat, part1 = sum a, with xhat rebuilt from x,
+// mean and rstd.  One launch covers up to kMaxColJobs reductions; workgroup
+// ranges are assigned to the jobs in order.
+struct ColPartialBatch {
+  ColPartialJob j[kMaxColJobs];
+  int start[kMaxColJobs + 1];  // first workgroup of each job
+  int n;
+};
+
 template <typename T, int MODE>
-__global__ void __launch_bounds__(256) segment_partials_kernel(int rows, int cols, const T* __restrict__ a,
-                                                               const T* __restrict__ x,
-                                                               const float* __restrict__ mean,
-                                                               const float* __restrict__ rstd,
-                                                               float* __restrict__ part0,
-                                                               float* __restrict__ part1) {
+__device__ __forceinline__ void segment_partials(const ColPartialJob& J, int cx, int seg,
+                                                 float (&red)[2][kRowsPerBlock][64 * 8]) {
   constexpr int NQ = MODE == 0 ? 1 : 2;
-  __shared__ float red[NQ][kRowsPerBlock][64 * 8];
+  const T* __restrict__ a = static_cast<const T*>(J.a);
+  const T* __restrict__ x = static_cast<const T*>(J.x);
   const int w = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
-  const int seg = blockIdx.y;
-  const int c = (blockIdx.x * 64 + lane) * 8;
+  const int c = (cx * 64 + lane) * 8;
   const int r0 = seg * kReduceRows;
-  const int r1 = min(r0 + kReduceRows, rows);
+  const int r1 = min(r0 + kReduceRows, J.rows);
   float acc[NQ][8];
 #pragma unroll
   for (int q = 0; q < NQ; ++q)
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[q][e] = 0.0f;
-  if (c < cols) {
+  if (c < J.cols) {
     for (int r = r0 + w; r < r1; r += kRowsPerBlock) {
       float v[8];
-      load8(a + (size_t)r * cols + c, v);
+      load8(a + (size_t)r * J.cols + c, v);
       if constexpr (MODE == 0) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc[0][e] += v[e];
       } else {
         float xv[8];
-        load8(x + (size_t)r * cols + c, xv);
-        const float mu = mean[r], rs = rstd[r];
+        load8(x + (size_t)r * J.cols + c, xv);
+        const float mu = J.mean[r], rs = J.rstd[r];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           acc[0][e] += v[e] * ((xv[e] - mu) * rs);
@@ -181,38 +184,63 @@ __global__ void __launch_bounds__(256) segment_partials_kernel(int rows, int col
   // 256 threads finish 64 lanes x 8 columns x NQ quantities; wave order fixed.
   for (int idx = threadIdx.x; idx < NQ * 64 * 8; idx += 256) {
     const int q = idx / (64 * 8);
-    const int j = idx % (64 * 8);
-    const int col = blockIdx.x * 64 * 8 + j;
-    if (col < cols) {
+    const int jc = idx % (64 * 8);
+    const int col = cx * 64 * 8 + jc;
+    if (col < J.cols) {
       float t = 0.0f;
 #pragma unroll
-      for (int i = 0; i < kRowsPerBlock; ++i) t += red[q][i][j];
-      (q == 0 ? part0 : part1)[(size_t)seg * cols + col] = t;
+      for (int i = 0; i < kRowsPerBlock; ++i) t += red[q][i][jc];
+      (q == 0 ? J.p0 : J.p1)[(size_t)seg * J.cols + col] = t;
     }
   }
 }
 
+template <typename T>
+__global__ void __launch_bounds__(256) segment_partials_kernel(ColPartialBatch b) {
+  __shared__ float red[2][kRowsPerBlock][64 * 8];
+  const int bid = blockIdx.x;
+  ColPartialJob J = b.j[0];
+  int s0 = 0;
+#pragma unroll
+  for (int i = 1; i < kMaxColJobs; ++i)
+    if (i < b.n && bid >= b.start[i]) { J = b.j[i]; s0 = b.start[i]; }
+  const int local = bid - s0;
+  const int ncx = (J.cols / 8 + 63) / 64;
+  if (J.mode == 0) segment_partials<T, 0>(J, local % ncx, local / ncx, red);
+  else segment_partials<T, 1>(J, local % ncx, local / ncx, red);
+}
+
 // out[c] (= or +=) sum_g part[g, c].  16 waves split the groups round-robin and
 // their sums are added in wave order, so the result does not depend on timing.
+// One launch covers up to kMaxColJobs such sums, 64 columns per workgroup.
 constexpr int kReduceWaves = 16;
-__global__ void __launch_bounds__(64 * kReduceWaves) reduce_partials_kernel(int groups, int cols,
-                                                                           const float* __restrict__ part,
-                                                                           float* __restrict__ out,
-                                                                           int accumulate) {
+struct ReduceBatch {
+  ReduceJob j[kMaxColJobs];
+  int start[kMaxColJobs + 1];
+  int n;
+};
+
+__global__ void __launch_bounds__(64 * kReduceWaves) reduce_partials_kernel(ReduceBatch b) {
   __shared__ float red[kReduceWaves][64];
+  const int bid = blockIdx.x;
+  ReduceJob J = b.j[0];
+  int s0 = 0;
+#pragma unroll
+  for (int i = 1; i < kMaxColJobs; ++i)
+    if (i < b.n && bid >= b.start[i]) { J = b.j[i]; s0 = b.start[i]; }
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
-  const int c = blockIdx.x * 64 + lane;
+  const int c = (bid - s0) * 64 + lane;
   float s = 0.0f;
-  if (c < cols)
-    for (int g = w; g < groups; g += kReduceWaves) s += part[(size_t)g * cols + c];
+  if (c < J.cols)
+    for (int g = w; g < J.groups; g += kReduceWaves) s += J.part[(size_t)g * J.cols + c];
   red[w][lane] = s;
   __syncthreads();
-  if (w == 0 && c < cols) {
+  if (w == 0 && c < J.cols) {
     float t = 0.0f;
 #pragma unroll
     for (int i = 0; i < kReduceWaves; ++i) t += red[i][lane];
-    out[c] = accumulate ? out[c] + t : t;
+    J.out[c] = J.accumulate ? J.out[c] + t : t;
   }
 }
 
@@ -298,38 +326,65 @@ hipError_t launch_layernorm_bwd(int dtype, int rows, int h, const void* dout, co
                           : ln_bwd_dispatch<float>(rm, h, dout, x, mean, rstd, gamma, dres, dx, stream);
 }
 
-template <int MODE>
-static hipError_t partials_launch(int dtype, int rows, int cols, const void* a, const void* x,
-                                  const float* mean, const float* rstd, float* p0, float* p1, hipStream_t s) {
-  if (rows <= 0) return hipSuccess;
-  if (cols % 8 != 0) return hipErrorInvalidValue;
-  dim3 grid((cols / 8 + 63) / 64, (unsigned)reduce_groups(rows));
+hipError_t launch_column_partials_batch(int dtype, const ColPartialJob* jobs, int n, hipStream_t stream) {
+  if (n < 1 || n > kMaxColJobs) return hipErrorInvalidValue;
+  ColPartialBatch b;
+  b.n = 0;
+  int total = 0;
+  for (int i = 0; i < n; ++i) {
+    const ColPartialJob& J = jobs[i];
+    if (J.rows <= 0 || J.cols <= 0) continue;
+    if (J.cols % 8 != 0 || (J.mode != 0 && J.mode != 1)) return hipErrorInvalidValue;
+    const long long wg = (long long)((J.cols / 8 + 63) / 64) * (long long)reduce_groups(J.rows);
+    if (total + wg > 0x7fffffffLL) return hipErrorInvalidValue;
+    b.j[b.n] = J;
+    b.start[b.n] = total;
+    total += (int)wg;
+    ++b.n;
+  }
+  if (b.n == 0) return hipSuccess;
+  b.start[b.n] = total;
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL((segment_partials_kernel<bf16_t, MODE>), grid, dim3(256), 0, s, rows, cols,
-                       (const bf16_t*)a, (const bf16_t*)x, mean, rstd, p0, p1);
+    hipLaunchKernelGGL(segment_partials_kernel<bf16_t>, dim3(total), dim3(256), 0, stream, b);
   else
-    hipLaunchKernelGGL((segment_partials_kernel<float, MODE>), grid, dim3(256), 0, s, rows, cols,
-                       (const float*)a, (const float*)x, mean, rstd, p0, p1);
+    hipLaunchKernelGGL(segment_partials_kernel<float>, dim3(total), dim3(256), 0, stream, b);
   return hipGetLastError();
 }
 
 hipError_t launch_column_partials(int dtype, int rows, int cols, const void* x, float* part, hipStream_t stream) {
-  return partials_launch<0>(dtype, rows, cols, x, nullptr, nullptr, nullptr, part, nullptr, stream);
+  const ColPartialJob j{0, rows, cols, x, nullptr, nullptr, nullptr, part, nullptr};
+  return launch_column_partials_batch(dtype, &j, 1, stream);
 }
 
 hipError_t launch_layernorm_param_partials(int dtype, int rows, int h, const void* dout, const void* x,
                                            const float* mean, const float* rstd, float* part_g, float* part_b,
                                            hipStream_t stream) {
-  return partials_launch<1>(dtype, rows, h, dout, x, mean, rstd, part_g, part_b, stream);
+  const ColPartialJob j{1, rows, h, dout, x, mean, rstd, part_g, part_b};
+  return launch_column_partials_batch(dtype, &j, 1, stream);
+}
+
+hipError_t launch_reduce_partials_batch(const ReduceJob* jobs, int n, hipStream_t stream) {
+  if (n < 1 || n > kMaxColJobs) return hipErrorInvalidValue;
+  ReduceBatch b;
+  b.n = 0;
+  int total = 0;
+  for (int i = 0; i < n; ++i) {
+    if (jobs[i].cols <= 0) continue;
+    b.j[b.n] = jobs[i];
+    b.start[b.n] = total;
+    total += (jobs[i].cols + 63) / 64;
+    ++b.n;
+  }
+  if (b.n == 0) return hipSuccess;
+  b.start[b.n] = total;
+  hipLaunchKernelGGL(reduce_partials_kernel, dim3(total), dim3(64 * kReduceWaves), 0, stream, b);
+  return hipGetLastError();
 }
 
 hipError_t launch_reduce_partials(int groups, int cols, const float* part, float* out, int accumulate,
                                   hipStream_t stream) {
-  if (cols <= 0) return hipSuccess;
-  dim3 grid((cols + 63) / 64);
-  hipLaunchKernelGGL(reduce_partials_kernel, grid, dim3(64 * kReduceWaves), 0, stream, groups, cols, part, out,
-                     accumulate);
-  return hipGetLastError();
+  const ReduceJob j{groups, cols, part, out, accumulate};
+  return launch_reduce_partials_batch(&j, 1, stream);
 }
 
 }  // namespace merak

@@ -437,8 +437,7 @@ int block_backward_step(merak_stage* S, const void* params, int l, int j, int k,
 // bias reductions on st_b and its LayerNorm reductions on st_ln (all three may
 // be the same stream; each must already follow the whole chain).
 int block_param_grads(merak_stage* S, int l, int group, const char* A, const char* x, const char* dy, const char* B,
-                      const char* d_ln1, const char* d_ln2, float* grads, int acc, hipStream_t st,
-                      hipStream_t st_b = nullptr, hipStream_t st_ln = nullptr) {
+                      const char* d_ln1, const char* d_ln2, float* grads, int acc, hipStream_t st) {
   const Dims& D = S->D;
   const ActLayout& L = S->W.act;
   const BwdLayout& Bl = S->W.bwd;
@@ -446,20 +445,21 @@ int block_param_grads(merak_stage* S, int l, int group, const char* A, const cha
   const int T = D.T;
   const int G = (int)reduce_groups(T);
   float* g = grads + S->p_stride * l;
-  float* pb;
+  auto part = [&](size_t off) { return (float*)(B + off); };
   if (group == 0) {
     // dW = dY^T X for FC2 and FC1, one grouped launch
     GemmProblem p[2];
     p[0] = gp(D.h, D.fl, T, dy, D.h, A + L.g, D.fl, g + S->p_off[P_W2], D.fl, nullptr, nullptr, nullptr, acc);
     p[1] = gp(D.fl, D.h, T, B + Bl.du, D.fl, A + L.ln2, D.h, g + S->p_off[P_W1], D.h, nullptr, nullptr, nullptr, acc);
     LAUNCH(MERAK_KC_GEMM_DW, st, launch_gemm(dt, true, true, EPI_F32, p, 2, st));
-    // bias gradients: token sums of the layer output gradients
-    pb = (float*)(B + Bl.p_b2);
-    LAUNCH(MERAK_KC_REDUCE, st, launch_column_partials(dt, T, D.h, dy, pb, st));
-    LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials(G, D.h, pb, g + S->p_off[P_B2], acc, st));
-    pb = (float*)(B + Bl.p_b1);
-    LAUNCH(MERAK_KC_REDUCE, st, launch_column_partials(dt, T, D.fl, B + Bl.du, pb, st));
-    LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials(G, D.fl, pb, g + S->p_off[P_B1], acc, st));
+    // bias gradients: token sums of the layer output gradients (one launch
+    // for the partials, one for the final sums)
+    const ColPartialJob cj[2] = {{0, T, D.h, dy, nullptr, nullptr, nullptr, part(Bl.p_b2), nullptr},
+                                 {0, T, D.fl, B + Bl.du, nullptr, nullptr, nullptr, part(Bl.p_b1), nullptr}};
+    LAUNCH(MERAK_KC_REDUCE, st, launch_column_partials_batch(dt, cj, 2, st));
+    const ReduceJob rj[2] = {{G, D.h, part(Bl.p_b2), g + S->p_off[P_B2], acc},
+                             {G, D.fl, part(Bl.p_b1), g + S->p_off[P_B1], acc}};
+    LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials_batch(rj, 2, st));
     return MERAK_OK;
   }
   GemmProblem p[2];
@@ -467,29 +467,21 @@ int block_param_grads(merak_stage* S, int l, int group, const char* A, const cha
             nullptr, acc);
   p[1] = gp(D.h, D.hl, T, B + Bl.dx1, D.h, A + L.o, D.hl, g + S->p_off[P_WO], D.hl, nullptr, nullptr, nullptr, acc);
   LAUNCH(MERAK_KC_GEMM_DW_ATTN, st, launch_gemm(dt, true, true, EPI_F32, p, 2, st));
-  if (!st_b) st_b = st;
-  if (!st_ln) st_ln = st;
-  st = st_b;
-  pb = (float*)(B + Bl.p_bqkv);
-  LAUNCH(MERAK_KC_REDUCE, st, launch_column_partials(dt, T, 3 * D.hl, B + Bl.dqkv, pb, st));
-  LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials(G, 3 * D.hl, pb, g + S->p_off[P_BQKV], acc, st));
-  pb = (float*)(B + Bl.p_bo);
-  LAUNCH(MERAK_KC_REDUCE, st, launch_column_partials(dt, T, D.h, B + Bl.dx1, pb, st));
-  LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials(G, D.h, pb, g + S->p_off[P_BO], acc, st));
-  // LayerNorm parameters
-  st = st_ln;
-  float* pg = (float*)(B + Bl.p_g2);
-  float* pbe = (float*)(B + Bl.p_be2);
-  LAUNCH(MERAK_KC_REDUCE, st, launch_layernorm_param_partials(dt, T, D.h, d_ln2, A + L.x1, (const float*)(A + L.mu2),
-                                          (const float*)(A + L.rs2), pg, pbe, st));
-  LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials(G, D.h, pg, g + S->p_off[P_LN2G], acc, st));
-  LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials(G, D.h, pbe, g + S->p_off[P_LN2B], acc, st));
-  pg = (float*)(B + Bl.p_g1);
-  pbe = (float*)(B + Bl.p_be1);
-  LAUNCH(MERAK_KC_REDUCE, st, launch_layernorm_param_partials(dt, T, D.h, d_ln1, x, (const float*)(A + L.mu1),
-                                          (const float*)(A + L.rs1), pg, pbe, st));
-  LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials(G, D.h, pg, g + S->p_off[P_LN1G], acc, st));
-  LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials(G, D.h, pbe, g + S->p_off[P_LN1B], acc, st));
+  // QKV and projection biases, both LayerNorms' parameters
+  const ColPartialJob cj[4] = {
+      {0, T, 3 * D.hl, B + Bl.dqkv, nullptr, nullptr, nullptr, part(Bl.p_bqkv), nullptr},
+      {0, T, D.h, B + Bl.dx1, nullptr, nullptr, nullptr, part(Bl.p_bo), nullptr},
+      {1, T, D.h, d_ln2, A + L.x1, (const float*)(A + L.mu2), (const float*)(A + L.rs2), part(Bl.p_g2),
+       part(Bl.p_be2)},
+      {1, T, D.h, d_ln1, x, (const float*)(A + L.mu1), (const float*)(A + L.rs1), part(Bl.p_g1), part(Bl.p_be1)}};
+  LAUNCH(MERAK_KC_REDUCE, st, launch_column_partials_batch(dt, cj, 4, st));
+  const ReduceJob rj[6] = {{G, 3 * D.hl, part(Bl.p_bqkv), g + S->p_off[P_BQKV], acc},
+                           {G, D.h, part(Bl.p_bo), g + S->p_off[P_BO], acc},
+                           {G, D.h, part(Bl.p_g2), g + S->p_off[P_LN2G], acc},
+                           {G, D.h, part(Bl.p_be2), g + S->p_off[P_LN2B], acc},
+                           {G, D.h, part(Bl.p_g1), g + S->p_off[P_LN1G], acc},
+                           {G, D.h, part(Bl.p_be1), g + S->p_off[P_LN1B], acc}};
+  LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials_batch(rj, 6, st));
   return MERAK_OK;
 }
 
@@ -794,16 +786,7 @@ int merak_stage_bwd(merak_stage_t S, const void* params, const void* dy, void* d
         HIP_TRY(hipEventRecord(S->ev_j1, s1));
         HIP_TRY(hipStreamWaitEvent(S->aux, S->ev_j0, 0));
         HIP_TRY(hipStreamWaitEvent(S->aux, S->ev_j1, 0));
-        if (k == 0 || l > 0) {
-          TRY(block_param_grads(S, l, k == 0 ? 0 : 1, A, xin, dyl, B, d1, d2, grads, accumulate, S->aux));
-        } else {
-          // Last block: the chains are done, so s0 and s1 take the bias and
-          // LayerNorm reductions beside the weight-gradient GEMM instead of
-          // queueing them after it on the internal stream.
-          HIP_TRY(hipStreamWaitEvent(s0, S->ev_j1, 0));
-          HIP_TRY(hipStreamWaitEvent(s1, S->ev_j0, 0));
-          TRY(block_param_grads(S, l, 1, A, xin, dyl, B, d1, d2, grads, accumulate, S->aux, s0, s1));
-        }
+        TRY(block_param_grads(S, l, k == 0 ? 0 : 1, A, xin, dyl, B, d1, d2, grads, accumulate, S->aux));
       }
     }
     HIP_TRY(hipEventRecord(S->ev_dw[par], S->aux));
