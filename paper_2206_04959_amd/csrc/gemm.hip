@@ -84,6 +84,60 @@ __device__ __forceinline__ void epilogue4(const GemmProblem& p, int m, int n, fl
   }
 }
 
+// ---------------------------------------------------------------------------
+// Epilogue on 8 consecutive columns n..n+7 of row m (16-byte bf16 / 32-byte
+// fp32 accesses).
+// ---------------------------------------------------------------------------
+template <typename T, int EPI>
+__device__ __forceinline__ void epilogue8(const GemmProblem& p, int m, int n, float v[8]) {
+  const size_t off = (size_t)m * p.ldc + n;
+  if constexpr (EPI == EPI_F32) {
+    float* c = reinterpret_cast<float*>(p.c) + off;
+    if (p.accumulate) {
+      float o[8];
+      load8(c, o);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] += o[e];
+    }
+    store8(c, v);
+  } else {
+    T* c = reinterpret_cast<T*>(p.c) + off;
+    if constexpr (EPI == EPI_STORE) {
+      store8(c, v);
+    } else if constexpr (EPI == EPI_BIAS) {
+      float b[8];
+      load8(reinterpret_cast<const T*>(p.bias) + n, b);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] += b[e];
+      store8(c, v);
+    } else if constexpr (EPI == EPI_BIAS_GELU) {
+      float b[8], g[8];
+      load8(reinterpret_cast<const T*>(p.bias) + n, b);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        v[e] += b[e];
+        g[e] = gelu_f(v[e]);
+      }
+      store8(reinterpret_cast<T*>(p.aux) + off, v);
+      store8(c, g);
+    } else if constexpr (EPI == EPI_BIAS_RESID) {
+      float b[8], r[8];
+      if (p.aux) store8(reinterpret_cast<T*>(p.aux) + off, v);
+      load8(reinterpret_cast<const T*>(p.bias) + n, b);
+      load8(reinterpret_cast<const T*>(p.resid) + off, r);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = r[e] + v[e] + b[e];
+      store8(c, v);
+    } else if constexpr (EPI == EPI_GELU_BWD) {
+      float u[8];
+      load8(reinterpret_cast<const T*>(p.aux) + off, u);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] *= gelu_grad_f(u[e]);
+      store8(c, v);
+    }
+  }
+}
+
 // Problem owning workgroup `bid`, copied out with uniform selects (a dynamic
 // index into the kernel-argument struct would go through scratch memory).
 __device__ __forceinline__ GemmProblem select_problem(const GemmBatch& b, int bid, int* start) {
@@ -336,30 +390,6 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_mfma_kernel(GemmBatch batch
     if (kt + NS < KT) issue(cur);
     step(smem + ((kt + 1) % NS) * STAGE, 0, a0, b0, a1, b1);
   }
-  // acc[j][i][r]: output row m = m0 + wm*WTM + i*32 + lane%32,
-  // column n = n0 + wn*WTN + j*32 + (r/4)*8 + (lane/32)*4 + r%4.
-  auto out_m = [&](int i) { return m0 + wm * WTM + i * 32 + (lane & 31); };
-  auto out_n = [&](int j, int g) { return n0 + wn * WTN + j * 32 + g * 8 + (lane >> 5) * 4; };
-
-  // Epilogues that read a [M, N] operand (the residual, or the stored GeLU
-  // input u) fetch it before the last K stage, so the loads overlap its MFMAs
-  // (wave tiles of up to six 32 x 32 blocks: 48 extra registers).
-  constexpr bool PRE = (EPI == EPI_BIAS_RESID || EPI == EPI_GELU_BWD) && TM * TN <= 6;
-  u32x2_t pre[PRE ? TN : 1][PRE ? TM : 1][4];
-  if constexpr (PRE) {
-    const bf16_t* src = reinterpret_cast<const bf16_t*>(EPI == EPI_BIAS_RESID ? p.resid : p.aux);
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int m = out_m(i), n = out_n(j, g);
-          pre[j][i][g] = (m < p.M && n < p.N) ? *reinterpret_cast<const u32x2_t*>(src + (size_t)m * p.ldc + n)
-                                              : u32x2_t{0u, 0u};
-        }
-  }
-
   {
     const char* st = smem + ((KT - 1) % NS) * STAGE;
     step(st, 1, a1, b1, a0, b0);
@@ -367,41 +397,44 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_mfma_kernel(GemmBatch batch
     step(st, 3, a1, b1, a0, b0);
     mfmas(a1, b1);
   }
+  // acc[j][i][r]: output row m = m0 + wm*WTM + i*32 + lane%32,
+  // column n = n0 + wn*WTN + j*32 + (r/4)*8 + (lane/32)*4 + r%4.
+  // Epilogue through LDS, one 32-row slab of the wave tile at a time: the
+  // accumulators (row = lane % 32, four columns per register quad) go to a
+  // padded fp32 staging tile, and are read back as 8 consecutive columns per
+  // lane, so that consecutive lanes cover contiguous row segments of C and of
+  // the epilogue's operands (16-byte accesses instead of 8-byte pieces of 32
+  // rows).
+  constexpr int CLD = WTN + 4;  // staging row, fp32
+  static_assert((size_t)NW * 32 * CLD * 4 <= (size_t)NS * STAGE, "epilogue staging fits in the operand ring");
+  float* stg = reinterpret_cast<float*>(smem) + wave * 32 * CLD;
+  constexpr int CPR = WTN / 8;  // 8-column chunks per row
+  __syncthreads();  // every wave has finished reading operand tiles
 #pragma unroll
-  for (int j = 0; j < TN; ++j)
+  for (int i = 0; i < TM; ++i) {
 #pragma unroll
-    for (int i = 0; i < TM; ++i) {
-      const int m = out_m(i);
-      if (m >= p.M) continue;
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int n = out_n(j, g);
-        if (n < p.N) {
-          float v[4] = {acc[j][i][4 * g], acc[j][i][4 * g + 1], acc[j][i][4 * g + 2], acc[j][i][4 * g + 3]};
-          if constexpr (PRE) {
-            const u32x2_t w = pre[j][i][g];
-            const float x[4] = {__uint_as_float(w[0] << 16), __uint_as_float(w[0] & 0xffff0000u),
-                                __uint_as_float(w[1] << 16), __uint_as_float(w[1] & 0xffff0000u)};
-            bf16_t* c = reinterpret_cast<bf16_t*>(p.c) + (size_t)m * p.ldc + n;
-            if constexpr (EPI == EPI_BIAS_RESID) {
-              if (p.aux) store4(reinterpret_cast<bf16_t*>(p.aux) + (size_t)m * p.ldc + n, v);
-              float b[4];
-              load4(reinterpret_cast<const bf16_t*>(p.bias) + n, b);
+      for (int g = 0; g < 4; ++g)
+        *reinterpret_cast<f32x4_t*>(stg + (lane & 31) * CLD + j * 32 + g * 8 + (lane >> 5) * 4) =
+            f32x4_t{acc[j][i][4 * g], acc[j][i][4 * g + 1], acc[j][i][4 * g + 2], acc[j][i][4 * g + 3]};
+    __syncthreads();
 #pragma unroll
-              for (int e = 0; e < 4; ++e) v[e] = x[e] + v[e] + b[e];
-            } else {
-#pragma unroll
-              for (int e = 0; e < 4; ++e) v[e] *= gelu_grad_f(x[e]);
-            }
-            store4(c, v);
-          } else {
-            epilogue4<bf16_t, EPI>(p, m, n, v);
-          }
-        }
+    for (int q = lane; q < 32 * CPR; q += 64) {
+      const int r = q / CPR, cc = q % CPR;
+      const int m = m0 + wm * WTM + i * 32 + r;
+      const int n = n0 + wn * WTN + cc * 8;
+      if (m < p.M && n < p.N) {
+        float v[8];
+        const f32x4_t lo = *reinterpret_cast<const f32x4_t*>(stg + r * CLD + cc * 8);
+        const f32x4_t hi = *reinterpret_cast<const f32x4_t*>(stg + r * CLD + cc * 8 + 4);
+        v[0] = lo[0]; v[1] = lo[1]; v[2] = lo[2]; v[3] = lo[3];
+        v[4] = hi[0]; v[5] = hi[1]; v[6] = hi[2]; v[7] = hi[3];
+        epilogue8<bf16_t, EPI>(p, m, n, v);
       }
-      // one output block at a time (keeps the accumulators in place)
-      __builtin_amdgcn_sched_barrier(0);
     }
+    __syncthreads();  // the slab is read before the next one overwrites it
+  }
 }
 
 // ---------------------------------------------------------------------------
