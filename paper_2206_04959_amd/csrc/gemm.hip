@@ -88,8 +88,11 @@ __device__ __forceinline__ void epilogue4(const GemmProblem& p, int m, int n, fl
 // Epilogue on 8 consecutive columns n..n+7 of row m (16-byte bf16 / 32-byte
 // fp32 accesses).
 // ---------------------------------------------------------------------------
+// `pre`, when given, holds the [M, N] operand the epilogue reads (the residual,
+// or the stored GeLU input), fetched ahead of time.
 template <typename T, int EPI>
-__device__ __forceinline__ void epilogue8(const GemmProblem& p, int m, int n, float v[8]) {
+__device__ __forceinline__ void epilogue8(const GemmProblem& p, int m, int n, float v[8],
+                                          const u32x4_t* pre = nullptr) {
   const size_t off = (size_t)m * p.ldc + n;
   if constexpr (EPI == EPI_F32) {
     float* c = reinterpret_cast<float*>(p.c) + off;
@@ -124,13 +127,15 @@ __device__ __forceinline__ void epilogue8(const GemmProblem& p, int m, int n, fl
       float b[8], r[8];
       if (p.aux) store8(reinterpret_cast<T*>(p.aux) + off, v);
       load8(reinterpret_cast<const T*>(p.bias) + n, b);
-      load8(reinterpret_cast<const T*>(p.resid) + off, r);
+      if (pre) unpack8(*pre, r);
+      else load8(reinterpret_cast<const T*>(p.resid) + off, r);
 #pragma unroll
       for (int e = 0; e < 8; ++e) v[e] = r[e] + v[e] + b[e];
       store8(c, v);
     } else if constexpr (EPI == EPI_GELU_BWD) {
       float u[8];
-      load8(reinterpret_cast<const T*>(p.aux) + off, u);
+      if (pre) unpack8(*pre, u);
+      else load8(reinterpret_cast<const T*>(p.aux) + off, u);
 #pragma unroll
       for (int e = 0; e < 8; ++e) v[e] *= gelu_grad_f(u[e]);
       store8(c, v);
@@ -390,6 +395,24 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_mfma_kernel(GemmBatch batch
     if (kt + NS < KT) issue(cur);
     step(smem + ((kt + 1) % NS) * STAGE, 0, a0, b0, a1, b1);
   }
+  // Epilogues that read a [M, N] operand fetch this lane's chunks of it for
+  // the first 32-row slab (in the row-contiguous layout of the staged epilogue
+  // below) before the last K stage, so that the loads overlap its MFMAs.
+  constexpr int CPR = WTN / 8;          // 8-column chunks per row of a wave tile
+  constexpr int CPL = 32 * CPR / 64;    // chunks per lane in a 32-row slab
+  static_assert((32 * CPR) % 64 == 0, "whole chunks per lane");
+  constexpr bool PRE = (EPI == EPI_BIAS_RESID || EPI == EPI_GELU_BWD) && CPL <= 8;
+  u32x4_t pre[PRE ? CPL : 1];
+  if constexpr (PRE) {
+    const bf16_t* src = reinterpret_cast<const bf16_t*>(EPI == EPI_BIAS_RESID ? p.resid : p.aux);
+#pragma unroll
+    for (int u = 0; u < CPL; ++u) {
+      const int q = lane + 64 * u;
+      const int m = m0 + wm * WTM + q / CPR, n = n0 + wn * WTN + (q % CPR) * 8;
+      pre[u] = (m < p.M && n < p.N) ? *reinterpret_cast<const u32x4_t*>(src + (size_t)m * p.ldc + n)
+                                     : u32x4_t{0u, 0u, 0u, 0u};
+    }
+  }
   {
     const char* st = smem + ((KT - 1) % NS) * STAGE;
     step(st, 1, a1, b1, a0, b0);
@@ -408,7 +431,6 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_mfma_kernel(GemmBatch batch
   constexpr int CLD = WTN + 4;  // staging row, fp32
   static_assert((size_t)NW * 32 * CLD * 4 <= (size_t)NS * STAGE, "epilogue staging fits in the operand ring");
   float* stg = reinterpret_cast<float*>(smem) + wave * 32 * CLD;
-  constexpr int CPR = WTN / 8;  // 8-column chunks per row
   __syncthreads();  // every wave has finished reading operand tiles
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
@@ -420,7 +442,8 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_mfma_kernel(GemmBatch batch
             f32x4_t{acc[j][i][4 * g], acc[j][i][4 * g + 1], acc[j][i][4 * g + 2], acc[j][i][4 * g + 3]};
     __syncthreads();
 #pragma unroll
-    for (int q = lane; q < 32 * CPR; q += 64) {
+    for (int u = 0; u < CPL; ++u) {
+      const int q = lane + 64 * u;
       const int r = q / CPR, cc = q % CPR;
       const int m = m0 + wm * WTM + i * 32 + r;
       const int n = n0 + wn * WTN + cc * 8;
@@ -430,7 +453,8 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_mfma_kernel(GemmBatch batch
         const f32x4_t hi = *reinterpret_cast<const f32x4_t*>(stg + r * CLD + cc * 8 + 4);
         v[0] = lo[0]; v[1] = lo[1]; v[2] = lo[2]; v[3] = lo[3];
         v[4] = hi[0]; v[5] = hi[1]; v[6] = hi[2]; v[7] = hi[3];
-        epilogue8<bf16_t, EPI>(p, m, n, v);
+        if constexpr (PRE) epilogue8<bf16_t, EPI>(p, m, n, v, i == 0 ? &pre[u] : nullptr);
+        else epilogue8<bf16_t, EPI>(p, m, n, v);
       }
     }
     __syncthreads();  // the slab is read before the next one overwrites it
