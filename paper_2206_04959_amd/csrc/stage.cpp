@@ -431,11 +431,11 @@ int block_backward_step(merak_stage* S, const void* params, int l, int j, int k,
 }
 
 // Weight, bias and LayerNorm gradients of block l over the whole micro-batch,
-// in two groups: group 0 (W2, b2, W1, b1) needs only dy and du, i.e. the FC2
-// backward of every sub-micro-batch; group 1 (W_o, b_o, W_qkv, b_qkv and both
-// LayerNorms) needs the rest of the chain.  The GEMMs go on st; group 1's
-// bias reductions on st_b and its LayerNorm reductions on st_ln (all three may
-// be the same stream; each must already follow the whole chain).
+// on stream st, in three parts that can start as soon as the chain has made
+// their inputs: part 0 (dW2, dW1, db2, db1) needs dy and du, i.e. the FC2
+// backward of every sub-micro-batch; part 1 (dW_o, dW_qkv) needs dx1 and dqkv,
+// i.e. the attention backward; part 2 (b_o, b_qkv and both LayerNorms' sums)
+// needs d_ln1, made by the QKV backward.
 int block_param_grads(merak_stage* S, int l, int group, const char* A, const char* x, const char* dy, const char* B,
                       const char* d_ln1, const char* d_ln2, float* grads, int acc, hipStream_t st) {
   const Dims& D = S->D;
@@ -462,11 +462,14 @@ int block_param_grads(merak_stage* S, int l, int group, const char* A, const cha
     LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials_batch(rj, 2, st));
     return MERAK_OK;
   }
-  GemmProblem p[2];
-  p[0] = gp(3 * D.hl, D.h, T, B + Bl.dqkv, 3 * D.hl, A + L.ln1, D.h, g + S->p_off[P_WQKV], D.h, nullptr, nullptr,
-            nullptr, acc);
-  p[1] = gp(D.h, D.hl, T, B + Bl.dx1, D.h, A + L.o, D.hl, g + S->p_off[P_WO], D.hl, nullptr, nullptr, nullptr, acc);
-  LAUNCH(MERAK_KC_GEMM_DW_ATTN, st, launch_gemm(dt, true, true, EPI_F32, p, 2, st));
+  if (group == 1) {
+    GemmProblem p[2];
+    p[0] = gp(3 * D.hl, D.h, T, B + Bl.dqkv, 3 * D.hl, A + L.ln1, D.h, g + S->p_off[P_WQKV], D.h, nullptr, nullptr,
+              nullptr, acc);
+    p[1] = gp(D.h, D.hl, T, B + Bl.dx1, D.h, A + L.o, D.hl, g + S->p_off[P_WO], D.hl, nullptr, nullptr, nullptr, acc);
+    LAUNCH(MERAK_KC_GEMM_DW_ATTN, st, launch_gemm(dt, true, true, EPI_F32, p, 2, st));
+    return MERAK_OK;
+  }
   // QKV and projection biases, both LayerNorms' parameters
   const ColPartialJob cj[4] = {
       {0, T, 3 * D.hl, B + Bl.dqkv, nullptr, nullptr, nullptr, part(Bl.p_bqkv), nullptr},
@@ -781,12 +784,15 @@ int merak_stage_bwd(merak_stage_t S, const void* params, const void* dy, void* d
           }
         }
       }
-      if (k == 0 || k == kChainSteps - 1) {
+      // Parameter gradients on the internal stream once every sub-micro-
+      // batch has passed the step that makes their inputs.
+      const int part = k == 0 ? 0 : k == 4 ? 1 : k == 5 ? 2 : -1;
+      if (part >= 0) {
         HIP_TRY(hipEventRecord(S->ev_j0, s0));
         HIP_TRY(hipEventRecord(S->ev_j1, s1));
         HIP_TRY(hipStreamWaitEvent(S->aux, S->ev_j0, 0));
         HIP_TRY(hipStreamWaitEvent(S->aux, S->ev_j1, 0));
-        TRY(block_param_grads(S, l, k == 0 ? 0 : 1, A, xin, dyl, B, d1, d2, grads, accumulate, S->aux));
+        TRY(block_param_grads(S, l, part, A, xin, dyl, B, d1, d2, grads, accumulate, S->aux));
       }
     }
     HIP_TRY(hipEventRecord(S->ev_dw[par], S->aux));
