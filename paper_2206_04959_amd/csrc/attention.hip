@@ -484,9 +484,10 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_bf16(int S, int H, int Bm, 
 template <int D>
 __global__ void __launch_bounds__(256) attn_bwd_dq_bf16(int S, int H, int Bm, int mstride,
                                                         const bf16_t* __restrict__ qkv,
+                                                        const bf16_t* __restrict__ o,
                                                         const bf16_t* __restrict__ dout,
                                                         const float* __restrict__ lse,
-                                                        const float* __restrict__ delta,
+                                                        float* __restrict__ delta,
                                                         bf16_t* __restrict__ dqkv, float scale_log2, float scale) {
   using TT = AttnTile<D>;
   constexpr int LD = TT::LD, KS = D / 16, DT = D / 32, TB = TT::BYTES;
@@ -513,7 +514,24 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_bf16(int S, int H, int Bm, in
     of[ks] = frag_kc(dOp + (size_t)q * ors + ks * 16 + hf * 8);
   }
   const float lse2 = lse[((size_t)b * H + hh) * S + q] * kLog2e;
-  const float del = delta[((size_t)b * H + hh) * S + q];
+  // delta = dO . O over the head dimension for this query: the lane holds
+  // half of the row's elements (the fragments above), lane ^ 32 the other
+  // half.  Written out for the dK/dV kernel, which runs after this one.
+  float del;
+  {
+    const bf16_t* Op = o + (size_t)b * S * ors + hh * D;
+    float part = 0.0f;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      float ov[8], dv[8];
+      load8(Op + (size_t)q * ors + ks * 16 + hf * 8, ov);
+      load8(dOp + (size_t)q * ors + ks * 16 + hf * 8, dv);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) part += dv[e] * ov[e];
+    }
+    del = part + __shfl_xor(part, 32, 64);
+    if (kh == 0 && hf == 0) delta[((size_t)b * H + hh) * S + q] = del;
+  }
   f32x16_t dq[DT];
 #pragma unroll
   for (int t = 0; t < DT; ++t)
@@ -727,8 +745,9 @@ __global__ void __launch_bounds__(128) attn_bwd_dkdv_f32(int B, int S, int H, co
                                                  const bf16_t* __restrict__, const float* __restrict__,          \
                                                  const float* __restrict__, bf16_t* __restrict__, float, float); \
   template __global__ void attn_bwd_dq_bf16<D>(int, int, int, int, const bf16_t* __restrict__,                   \
-                                               const bf16_t* __restrict__, const float* __restrict__,            \
-                                               const float* __restrict__, bf16_t* __restrict__, float, float);
+                                               const bf16_t* __restrict__, const bf16_t* __restrict__,           \
+                                               const float* __restrict__, float* __restrict__,                   \
+                                               bf16_t* __restrict__, float, float);
 MERAK_ATTN_INST(64)
 MERAK_ATTN_INST(96)
 MERAK_ATTN_INST(128)
@@ -781,12 +800,11 @@ static hipError_t bwd_d(int dtype, int B, int S, int H, int G, int mstride, cons
     hipError_t e = allow_lds(attn_bwd_dkdv_bf16<D>, lds_k, ok_k);
     if (e == hipSuccess) e = allow_lds(attn_bwd_dq_bf16<D>, lds_q, ok_q);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((attn_delta_kernel<bf16_t, D>), dim3((rows + 255) / 256), dim3(256), 0, st, G * B, S, H, B,
-                       mstride, (const bf16_t*)o, (const bf16_t*)dout, delta);
+    // dQ first: it also forms delta, which dK/dV reads.
     dim3 grid(H, G * B, S / 64);
-    hipLaunchKernelGGL((attn_bwd_dkdv_bf16<D>), grid, dim3(256), lds_k, st, S, H, B, mstride, (const bf16_t*)qkv,
-                       (const bf16_t*)dout, lse, delta, (bf16_t*)dqkv, scale * kLog2e, scale);
     hipLaunchKernelGGL((attn_bwd_dq_bf16<D>), grid, dim3(256), lds_q, st, S, H, B, mstride, (const bf16_t*)qkv,
+                       (const bf16_t*)o, (const bf16_t*)dout, lse, delta, (bf16_t*)dqkv, scale * kLog2e, scale);
+    hipLaunchKernelGGL((attn_bwd_dkdv_bf16<D>), grid, dim3(256), lds_k, st, S, H, B, mstride, (const bf16_t*)qkv,
                        (const bf16_t*)dout, lse, delta, (bf16_t*)dqkv, scale * kLog2e, scale);
   } else {
     hipLaunchKernelGGL((attn_delta_kernel<float, D>), dim3((rows + 255) / 256), dim3(256), 0, st, G * B, S, H, B,
