@@ -191,7 +191,7 @@ typedef enum {
   MERAK_KC_GEMM_DX = 2,    /* input-gradient GEMMs of the backward pass                  */
   MERAK_KC_GEMM_DW = 3,    /* weight-gradient GEMMs of FC1 and FC2, one launch per block */
   MERAK_KC_ATTN_FWD = 4,   /* attention forward                                          */
-  MERAK_KC_ATTN_BWD = 5,   /* attention backward (delta, dK/dV and dQ kernels)           */
+  MERAK_KC_ATTN_BWD = 5,   /* attention backward (dQ with delta, then dK/dV kernels)     */
   MERAK_KC_LN_FWD = 6,     /* LayerNorm forward                                          */
   MERAK_KC_LN_BWD = 7,     /* LayerNorm backward (input gradient)                        */
   MERAK_KC_REDUCE = 8,     /* bias / LayerNorm parameter gradient reductions             */
