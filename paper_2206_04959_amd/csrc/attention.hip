@@ -180,21 +180,8 @@ __global__ void __launch_bounds__(256) attn_fwd_bf16(int S, int H, int Bm, int m
     for (int r = 0; r < 16; ++r) oacc[t][r] = 0.0f;
   float m = -INFINITY, l = 0.0f;
 
-  if (kAttnStages == 2) load_stage(0, 0);
-  for (int it = 0; it < n_it; ++it) {
-    const int cur = it % kAttnStages;
-    if (kAttnStages == 1) {
-      __syncthreads();  // every wave is done with the previous block pair
-      load_stage(it, 0);
-    }
-    __syncthreads();  // this block pair landed (and, with two stages, the other stage is free)
-    if (kAttnStages == 2 && it + 1 < n_it) load_stage(it + 1, (it + 1) % kAttnStages);
-    const int kb = 2 * it + kh, k0 = kb * 64;
-    if (kb >= n_kb || k0 > q0 + 31) continue;
-    const char* Kt = smem + (cur * 4 + kh) * TB;
-    const char* Vt = smem + (cur * 4 + 2 + kh) * TB;
-
-    f32x16_t s[2];
+  // S = K Q^T of key block kb (LDS tile Kt) for this wave's 32 queries.
+  auto scores = [&](const char* Kt, f32x16_t (&s)[2]) {
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
 #pragma unroll
@@ -204,6 +191,9 @@ __global__ void __launch_bounds__(256) attn_fwd_bf16(int S, int H, int Bm, int m
         s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_row<LD>(Kt, t * 32 + l32, ks * 16 + hf * 8), qf[ks],
                                                        s[t], 0, 0, 0);
     }
+  };
+  // Causal mask, online softmax and O^T += V^T P^T with key block kb (tile Vt).
+  auto softmax_pv = [&](const char* Vt, int k0, f32x16_t (&s)[2]) {
     // s[t][r]: key k0 + t*32 + (r/4)*8 + 4*hf + r%4, query q.  Only a block
     // that reaches past the wave's first query needs the causal mask.
     float mloc = -INFINITY;
@@ -255,6 +245,48 @@ __global__ void __launch_bounds__(256) attn_fwd_bf16(int S, int H, int Bm, int m
       for (int g = 0; g < 4; ++g)
         oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_tr<LD>(Vt, g * 16, dt * 32, lane), pb[g], oacc[dt],
                                                            0, 0, 0);
+  };
+
+  if constexpr (kAttnStages == 1 && D <= 96) {
+    // One LDS stage, with K and V on separate schedules: the next block
+    // pair's K tiles are fetched while this pair's softmax and P.V run, and
+    // its V tiles while the next S = K Q^T runs.  Waves 0-1 load the K tiles
+    // and waves 2-3 the V tiles; before a barrier that publishes tiles, only
+    // the waves that loaded them wait for their own loads.  (At d = 128 the
+    // scores held across the middle barrier would cost a wave per SIMD.)
+    auto barrier = [&](bool wait_own_loads) {
+      if (wait_own_loads) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    };
+    load_stage(0, 0);
+    for (int it = 0; it < n_it; ++it) {
+      const int kb = 2 * it + kh, k0 = kb * 64;
+      const bool active = kb < n_kb && k0 <= q0 + 31;
+      f32x16_t s[2];
+      barrier(wave < 2);  // K tiles of this pair landed
+      if (active) scores(smem + kh * TB, s);
+      barrier(wave >= 2);  // every wave is done with the K tiles; V tiles landed
+      if (wave < 2 && it + 1 < n_it) load_stage(it + 1, 0);
+      if (active) softmax_pv(smem + (2 + kh) * TB, k0, s);
+      barrier(false);  // every wave is done with the V tiles
+      if (wave >= 2 && it + 1 < n_it) load_stage(it + 1, 0);
+    }
+  } else {
+    if (kAttnStages == 2) load_stage(0, 0);
+    for (int it = 0; it < n_it; ++it) {
+      const int cur = it % kAttnStages;
+      if (kAttnStages == 1) {
+        __syncthreads();  // every wave is done with the previous block pair
+        load_stage(it, 0);
+      }
+      __syncthreads();  // this block pair landed (and, with two stages, the other stage is free)
+      if (kAttnStages == 2 && it + 1 < n_it) load_stage(it + 1, (it + 1) % kAttnStages);
+      const int kb = 2 * it + kh, k0 = kb * 64;
+      if (kb >= n_kb || k0 > q0 + 31) continue;
+      f32x16_t s[2];
+      scores(smem + (cur * 4 + kh) * TB, s);
+      softmax_pv(smem + (cur * 4 + 2 + kh) * TB, k0, s);
+    }
   }
 
   // Merge the two key halves of each query group (partial m, l, O^T).
