@@ -7,22 +7,23 @@
 // bf16 path (v_mfma_f32_32x32x16_bf16, fp32 softmax): flash-style tiling so the
 // seq x seq score matrix never reaches HBM (the method published as
 // FlashAttention, Dao et al. 2022; the gfx950 tiling below is our own).
-//   * forward: a workgroup owns 32*NW query rows of one (batch, head), a wave 32
-//     of them.  It computes the transposed score tile S^T = K Q^T so that each
-//     lane owns one query column; the online softmax then needs only a lane-half
-//     exchange, and the probabilities P^T stay in registers as the second
-//     operand of the O^T += V^T P^T product (K/V tiles of 64 keys in LDS, V
-//     stored transposed).
-//   * backward, deterministic (no atomics): a KV-parallel kernel (a wave owns
-//     32 keys, loops over 64-query tiles) accumulates dK and dV; a Q-parallel
-//     kernel (a wave owns 32 queries, loops over 64-key tiles) accumulates dQ.
-//     Both rebuild P from the stored lse.  delta_i = rowsum(dO_i * O_i) comes
-//     from a small preprocessing kernel.
+//   * forward: a workgroup owns 64 query rows of one (batch, head); its four
+//     waves are two groups of 32 rows times the even and odd 64-key blocks,
+//     merged at the end with the online-softmax merge.  A wave computes the
+//     transposed score tile S^T = K Q^T so that each lane owns one query
+//     column; the softmax then needs only a lane-half exchange, and P^T stays
+//     in registers as the second operand of O^T += V^T P^T.  K and V tiles sit
+//     in LDS in their natural [key][d] layout; V^T fragments come from
+//     transposing LDS reads.
+//   * backward, deterministic (no atomics): a Q-parallel kernel accumulates dQ
+//     and also forms delta_i = rowsum(dO_i * O_i) for its rows; a KV-parallel
+//     kernel, run after it, accumulates dK and dV.  Both rebuild P from the
+//     stored lse.
 // The 32x32 accumulator layout is: lane l holds column l%32 and rows
 // (r/4)*8 + (l/32)*4 + r%4 for r = 0..15.  When such an accumulator feeds the
 // next MFMA as its 16-deep operand, the MFMA's k index 8*(l/32)+e is taken to
 // mean row (e/4)*8 + (l/32)*4 + e%4 of that 16-row group; the other operand is
-// read from a transposed LDS copy with the same key order (two 8-byte reads).
+// read with transposing LDS reads in the same key order (two 8-byte reads).
 //
 // fp32 check mode: one thread per query (or key) row, fp32 throughout.
 #include <math.h>
@@ -325,7 +326,8 @@ __global__ void __launch_bounds__(256) attn_fwd_bf16(int S, int H, int Bm, int m
 }
 
 // ---------------------------------------------------------------------------
-// delta[b, h, i] = sum_d dO[b, i, h, d] * O[b, i, h, d]
+// delta[b, h, i] = sum_d dO[b, i, h, d] * O[b, i, h, d] (fp32 check mode; the
+// bf16 dQ kernel forms it itself)
 // ---------------------------------------------------------------------------
 template <typename T, int D>
 __global__ void __launch_bounds__(256) attn_delta_kernel(int B, int S, int H, int Bm, int mstride,
