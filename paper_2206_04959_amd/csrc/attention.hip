@@ -513,7 +513,8 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_bf16(int S, int H, int Bm, 
 // ---------------------------------------------------------------------------
 // bf16 backward: dQ (Q-parallel), the forward's layout: 64 query rows per
 // workgroup, 2 query groups x 2 key halves, K and V tiles of two key blocks per
-// stage, partial dQ sums added at the end.
+// stage, partial dQ sums added at the end.  It also writes delta for its rows,
+// which the dK/dV kernel launched after it reads.
 // ---------------------------------------------------------------------------
 template <int D>
 __global__ void __launch_bounds__(256) attn_bwd_dq_bf16(int S, int H, int Bm, int mstride,
