@@ -165,7 +165,6 @@ struct WsLayout {
   size_t fwd_tmp;     // activations of recomputed blocks during the forward pass
   size_t chain;       // 3 input-gradient buffers
   size_t par[2];      // backward scratch per parity
-  size_t rc_y;        // recompute's (unused) block output
   size_t total;
   size_t recompute_total;
   int keep_slot[kMaxBlocks];  // index among kept blocks, or -1
@@ -191,7 +190,6 @@ WsLayout ws_layout(const Dims& D) {
   W.chain = o; o += 3 * th;
   W.par[0] = o; o += W.bwd.size;
   W.par[1] = o; o += W.bwd.size;
-  W.rc_y = o; o += (W.n_rc > 0 ? th : 0);
   W.total = o;
   W.recompute_total = (size_t)W.n_rc * W.act.size;
   return W;
@@ -347,10 +345,13 @@ int block_forward_step(merak_stage* S, const void* params, int l, int j, int k, 
 // stream j mod 2, issued step by step; the GEMMs of one step of the
 // sub-micro-batches that share a stream go out as one grouped launch (they are
 // independent problems of the same shape, so each keeps its own result).
+// With y == nullptr (recomputation) the FC2 step is left out: its output is
+// the next block's input, which is already checkpointed, and the backward
+// needs only FC2's input g.
 int block_forward(merak_stage* S, const void* params, int l, char* A, const char* x, char* y, char* part_o,
                   char* part_f, hipStream_t s0, hipStream_t s1) {
   const Dims& D = S->D;
-  for (int k = 0; k < kFwdSteps; ++k) {
+  for (int k = 0; k < (y ? kFwdSteps : kFwdSteps - 1); ++k) {
     for (int par = 0; par < 2; ++par) {
       hipStream_t st = par ? s1 : s0;
       GemmProblem probs[kMaxGroup];
@@ -708,8 +709,7 @@ int merak_stage_recompute(merak_stage_t S, const void* params, void* stream0, vo
     if (!((D.mask >> l) & 1)) continue;
     char* A = block_acts(S, l, 1);
     const char* xin = block_input(S, l);
-    char* yout = S->ws + S->W.rc_y;  // the block output is already checkpointed
-    TRY(block_forward(S, params, l, A, xin, yout, nullptr, nullptr, s0, s1));
+    TRY(block_forward(S, params, l, A, xin, nullptr, nullptr, nullptr, s0, s1));  // everything but FC2
     // the backward of block l waits for these (it may run on other streams)
     HIP_TRY(hipEventRecord(S->ev_rc[l][0], s0));
     HIP_TRY(hipEventRecord(S->ev_rc[l][1], s1));

@@ -5,8 +5,10 @@ Per block forward, one rank's shard, T = b*s tokens:
   attention  2*b*(h/t)*s*(s+1)   (causal: Q K^T and P V over the lower triangle
                                   including the diagonal)
 The backward pass costs twice the forward (Sec. 5.1 of the paper takes the same
-ratio), and each recomputed block repeats its forward once.  Tile padding and
-the attention backward's rebuilding of P are not counted.
+ratio), and each recomputed block repeats its forward once, except the FC2 GEMM:
+its output is the next block's (checkpointed) input, and the backward needs
+only FC2's input, so the recomputation leaves it out.  Tile padding and the
+attention backward's rebuilding of P are not counted.
 """
 from __future__ import annotations
 
@@ -24,9 +26,15 @@ def recomputed_blocks(s: StageShape) -> int:
     return bin(s.recompute_mask).count("1")
 
 
+def fc2_forward_flops(s: StageShape) -> float:
+    return 2.0 * s.tokens * s.local_ffn * s.hidden
+
+
 def executed_flops(s: StageShape) -> float:
-    """Forward + recompute + backward of the whole stage for one micro-batch."""
-    return (3 * s.n_blocks + recomputed_blocks(s)) * block_forward_flops(s)
+    """Forward + recompute (all but FC2) + backward of the whole stage for one
+    micro-batch."""
+    return 3 * s.n_blocks * block_forward_flops(s) + recomputed_blocks(s) * (block_forward_flops(s)
+                                                                             - fc2_forward_flops(s))
 
 
 def model_flops(s: StageShape) -> float:

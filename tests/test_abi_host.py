@@ -86,9 +86,10 @@ def test_workspace_sizes_follow_recompute_mask():
     wsa, rca = B.workspace_bytes(B.make_config(base.replace(recompute_mask=0b111111)))
     assert rc0 == 0 and rc3 > 0 and rca == 2 * rc3
     # recomputing 3 of 6 blocks frees the activations of 3 blocks from the per-handle
-    # workspace and adds one transient set for the forward pass
+    # workspace and adds one transient set for the forward pass (the recomputation
+    # leaves out FC2, whose output is the checkpointed next-block input)
     act = rc3 // 3
-    assert ws0 - ws3 == 3 * act - act - (base.tokens * base.hidden * 2)
+    assert ws0 - ws3 == 3 * act - act
     assert ws3 > 0 and wsa < ws3
 
 
