@@ -153,8 +153,10 @@ int merak_stage_fwd(merak_stage_t stage, const void* params, const void* x, void
                     void* fwd_partials, void* stream0, void* stream1);
 
 /* Rebuild the activations of every block whose recompute bit is set, from the
- * block inputs kept by merak_stage_fwd, into the recompute area.  Results are
- * bit-identical to what the forward pass computed.  Needs no upstream gradient
+ * block inputs kept by merak_stage_fwd, into the recompute area: the block's
+ * forward up to FC2's input (FC2's output is the next block's kept input, and
+ * its backward needs only the input).  Results are bit-identical to what the
+ * forward pass computed.  Needs no upstream gradient
  * (early recomputation).  MERAK_ERR_ORDER if no forward pass is pending.  A
  * no-op (MERAK_OK) when the mask is 0.  params must hold the same values as in
  * the forward call.
