@@ -28,6 +28,8 @@
 // fp32 check mode: one thread per query (or key) row, fp32 throughout.
 #include <math.h>
 
+#include <atomic>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -788,13 +790,14 @@ MERAK_ATTN_INST(96)
 MERAK_ATTN_INST(128)
 #undef MERAK_ATTN_INST
 
-// Allow a kernel's dynamic LDS beyond the default limit (once per instantiation).
+// Allow a kernel's dynamic LDS beyond the default limit (once per instantiation;
+// the call is idempotent, so host threads racing on the first launch are harmless).
 template <typename K>
-static hipError_t allow_lds(K kern, size_t bytes, bool& done) {
-  if (done) return hipSuccess;
+static hipError_t allow_lds(K kern, size_t bytes, std::atomic<bool>& done) {
+  if (done.load(std::memory_order_acquire)) return hipSuccess;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
                                      (int)bytes);
-  if (e == hipSuccess) done = true;
+  if (e == hipSuccess) done.store(true, std::memory_order_release);
   return e;
 }
 
@@ -804,7 +807,7 @@ static hipError_t fwd_d(int dtype, int B, int S, int H, int G, int mstride, cons
   const float scale = 1.0f / sqrtf((float)D);
   if (dtype == DT_BF16) {
     constexpr size_t lds = attn_lds_bytes<D>();
-    static bool ok = false;
+    static std::atomic<bool> ok{false};
     hipError_t e = allow_lds(attn_fwd_bf16<D>, lds, ok);
     if (e != hipSuccess) return e;
     dim3 grid(H, G * B, S / 64);
@@ -831,7 +834,7 @@ static hipError_t bwd_d(int dtype, int B, int S, int H, int G, int mstride, cons
     constexpr size_t lds_q = attn_lds_bytes<D>();
     constexpr size_t lds_k = attn_lds_bytes<D>() + kAttnStages * 256 * sizeof(float);
     static_assert(lds_k <= 160 * 1024, "LDS budget");
-    static bool ok_k = false, ok_q = false;
+    static std::atomic<bool> ok_k{false}, ok_q{false};
     hipError_t e = allow_lds(attn_bwd_dkdv_bf16<D>, lds_k, ok_k);
     if (e == hipSuccess) e = allow_lds(attn_bwd_dq_bf16<D>, lds_q, ok_q);
     if (e != hipSuccess) return e;

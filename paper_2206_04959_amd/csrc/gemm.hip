@@ -18,6 +18,7 @@
 //
 // fp32 check mode: a plain LDS-tiled FMA kernel with the same layouts and
 // epilogues.
+#include <atomic>
 #include <type_traits>
 
 #include "common.h"
@@ -192,6 +193,32 @@ __device__ __forceinline__ int xcd_remap(int bid, int n) {
   return (x < rem ? x * (per + 1) : rem * (per + 1) + (x - rem) * per) + idx;
 }
 
+// One 16-byte-per-lane global -> LDS load: lane i writes LDS bytes
+// [lds_addr + 16 i, lds_addr + 16 i + 16).  Issued as inline assembly: the
+// compiler would otherwise treat every later LDS read that it cannot prove
+// disjoint from this store (the transposing reads among them) as dependent on
+// it and wait for all outstanding loads before that read, which would serialise
+// the prefetch of the next K stage with the MFMAs of the current one.  The
+// kernels order these loads themselves (wait_vm_barrier).  An M0 write needs
+// one wait state before an LDS-DMA load.
+typedef int32_t i32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ i32x4_t operand_rsrc_words(const void* p, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(p);
+  return i32x4_t{(int32_t)(uint32_t)a, (int32_t)(uint32_t)((a >> 32) & 0xffffu), (int32_t)bytes, 0x00020000};
+}
+
+__device__ __forceinline__ void lds_dma16(i32x4_t rsrc, uint32_t lds_addr, uint32_t voff) {
+  asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+               :
+               : "v"(voff), "s"(rsrc), "{m0}"(lds_addr)
+               : "memory");
+}
+
+__device__ __forceinline__ uint32_t lds_address(const char* p) {
+  return (uint32_t)(uintptr_t)(const MERAK_LDS char*)p;
+}
+
 // Global -> LDS loader of one operand.  Each wave issues kInst 16-byte-per-lane
 // loads per K stage.
 template <bool TRANS, int R, int NW>
@@ -222,19 +249,19 @@ struct TileLoader {
 
   // Issue load q of the current K stage into `lds` (R * 128 bytes); after the
   // last one (q = kInst - 1) the loader moves on to the next stage.
-  __device__ __forceinline__ void issue_one(__amdgpu_buffer_rsrc_t rsrc, char* lds, int wave, int q) {
-    const int slot = __builtin_amdgcn_readfirstlane((q * NW + wave) * 1024);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (MERAK_LDS void*)(lds + slot), 16, (int)voff[q], 0, 0, 0);
+  __device__ __forceinline__ void issue_one(i32x4_t rsrc, char* lds, int wave, int q) {
+    const uint32_t addr = __builtin_amdgcn_readfirstlane(lds_address(lds) + (q * NW + wave) * 1024);
+    lds_dma16(rsrc, addr, voff[q]);
     voff[q] += step;
   }
 
   // Issue the loads of the current K stage into `lds` (R * 128 bytes) and move
   // on to the next stage.
-  __device__ __forceinline__ void issue(__amdgpu_buffer_rsrc_t rsrc, char* lds, int wave) {
+  __device__ __forceinline__ void issue(i32x4_t rsrc, char* lds, int wave) {
 #pragma unroll
     for (int q = 0; q < kInst; ++q) {
-      const int slot = __builtin_amdgcn_readfirstlane((q * NW + wave) * 1024);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (MERAK_LDS void*)(lds + slot), 16, (int)voff[q], 0, 0, 0);
+      const uint32_t addr = __builtin_amdgcn_readfirstlane(lds_address(lds) + (q * NW + wave) * 1024);
+      lds_dma16(rsrc, addr, voff[q]);
       voff[q] += step;
     }
   }
@@ -317,8 +344,8 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_mfma_kernel(GemmBatch batch
                                : (uint32_t)(((size_t)(p.M - 1) * p.lda + p.K) * 2);
   const uint32_t b_bytes = B_T ? (uint32_t)(((size_t)(p.K - 1) * p.ldb + p.N) * 2)
                                : (uint32_t)(((size_t)(p.N - 1) * p.ldb + p.K) * 2);
-  const __amdgpu_buffer_rsrc_t ra = operand_rsrc(p.a, a_bytes);
-  const __amdgpu_buffer_rsrc_t rb = operand_rsrc(p.b, b_bytes);
+  const i32x4_t ra = operand_rsrc_words(p.a, a_bytes);
+  const i32x4_t rb = operand_rsrc_words(p.b, b_bytes);
 
   TileLoader<A_T, BM, NW> la;
   TileLoader<B_T, BN, NW> lb;
@@ -528,13 +555,11 @@ static hipError_t run_mfma(GemmBatch& batch, hipStream_t stream) {
   constexpr size_t lds = (size_t)NS * (BM + BN) * 128;
   static_assert(lds <= 160 * 1024, "LDS budget");
   auto kern = gemm_mfma_kernel<BM, BN, WM, WN, NS, AT, BT, EPI>;
-  static bool attr_set = false;  // per instantiation
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
+  // Once per instantiation; the initialisation of a function-local static is
+  // thread-safe, so concurrent first launches from several host threads agree.
+  static const hipError_t attr_err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (attr_err != hipSuccess) return attr_err;
   hipLaunchKernelGGL(kern, dim3(tiles), dim3(WM * WN * 64), lds, stream, batch);
   return hipGetLastError();
 }
@@ -567,7 +592,7 @@ enum TileCfg {
   TILE_256x192_W8_S2 = 10,  // 4x2 waves of 64x96
   TILE_COUNT = 11
 };
-static int g_tile_override = TILE_AUTO;
+static std::atomic<int> g_tile_override{TILE_AUTO};
 
 static long long tile_count(const GemmBatch& b, int bm, int bn) {
   long long t = 0;
@@ -575,28 +600,25 @@ static long long tile_count(const GemmBatch& b, int bm, int bn) {
   return t;
 }
 
-// Tile choice (measured on MI355X with random bf16 data, isolated and inside
-// the two-stream stage step).  Long reductions (K >= 4096: the weight
-// gradients over a whole micro-batch) with enough work run as 256 x 256 tiles
-// on 8 waves.  Otherwise 128 x 192 tiles (64 x 96 per wave, two workgroups per
-// CU): a per-sub-micro-batch layer of 2048 x 3072 gives 256 of them, one per CU
-// per stream, which beat 128 x 128 tiles by 4% over the whole stage step.
-// Small long-K problems fall back to 128 x 128 tiles.
-static int choose_tile(const GemmBatch& b) {
+// Tile choice (measured on MI355X with random bf16 data, isolated, as two
+// concurrent launches, and inside the two-stream stage step).  Large tiles on
+// 8 waves (two per SIMD) move the fewest operand bytes per FLOP through L2 and
+// LDS: the input-gradient GEMMs (B read in place from the [out, in] weights)
+// run as 256 x 256 tiles, every other GEMM with at least 128 such tiles as
+// 256 x 192 tiles.  Narrow problems (the projection's input gradient, N = h/t)
+// keep 128 x 192 tiles on 4 waves so that the grid still covers most CUs.
+// Against 128 x 192 tiles everywhere the stage step measured +6.3% (819 ->
+// 870 TFLOP/s); 256 x 256 tiles everywhere +3.6%, 256 x 192 everywhere +5.3%.
+static int choose_tile(const GemmBatch& b, bool a_t, bool b_t) {
   if (g_tile_override != TILE_AUTO) return g_tile_override;
-  int kmin = b.p[0].K;
-  for (int i = 1; i < b.n_probs; ++i) kmin = b.p[i].K < kmin ? b.p[i].K : kmin;
-  if (kmin >= 4096) {
-    if (tile_count(b, 256, 256) >= 512) return TILE_256x256_W8_S2;
-    if (tile_count(b, 128, 192) >= 256) return TILE_128x192_W4_S2;
-    return TILE_128x128_W4_S2;
-  }
+  if (!a_t && b_t && tile_count(b, 256, 256) >= 128) return TILE_256x256_W8_S2;
+  if (tile_count(b, 256, 192) >= 128) return TILE_256x192_W8_S2;
   return TILE_128x192_W4_S2;
 }
 
 template <bool AT, bool BT, int EPI>
 static hipError_t run_bf16(GemmBatch& batch, hipStream_t stream) {
-  switch (choose_tile(batch)) {
+  switch (choose_tile(batch, AT, BT)) {
     case TILE_256x256_W4_S2: return run_mfma<256, 256, 2, 2, 2, AT, BT, EPI>(batch, stream);
     case TILE_256x128_W4_S3: return run_mfma<256, 128, 2, 2, 3, AT, BT, EPI>(batch, stream);
     case TILE_128x256_W4_S3: return run_mfma<128, 256, 2, 2, 3, AT, BT, EPI>(batch, stream);
@@ -652,7 +674,5 @@ hipError_t launch_gemm(int dtype, bool a_t, bool b_t, int epi, const GemmProblem
 
 extern "C" int merak_gemm_tile_override(int cfg) {
   if (cfg < merak::TILE_AUTO || cfg >= merak::TILE_COUNT) return -1;
-  const int prev = merak::g_tile_override;
-  merak::g_tile_override = cfg;
-  return prev;
+  return merak::g_tile_override.exchange(cfg);
 }
