@@ -13,6 +13,14 @@ HBM when timing starts.
 Prints one JSON line (last line of stdout).
 
     python bench.py [--steps K] [--warmup W] [--config NAME] [--no-cpu-baseline]
+                    [--n-sub N] [--mask M] [--streams 1|2] [--class-steps C]
+
+`value` is executed FLOP per step over the mean step time of the K timed
+steps (per-kernel timing off); the median and p10/p90 step times come from an
+event per step boundary.  `roofline` is the kernel class with the largest
+summed launch time per step, timed afterwards in a separate loop with HIP
+events around every launch of one class at a time (on the stream each launch
+runs on); `kernel_classes` lists every class.
 """
 from __future__ import annotations
 
@@ -30,8 +38,9 @@ from paper_2206_04959_amd import flops, synth  # noqa: E402
 
 METRIC = "stage-shard fwd+bwd TFLOP/s per MI355X and % bf16 MFMA peak (8.3B-shaped, t=4)"
 PEAK_BF16_TFLOPS = 2516.6   # dense bf16 MFMA: 256 CUs x 4096 FLOP/clk x 2.4 GHz
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_dw_traffic.json")
-GEMM_SOURCE = os.path.join(ROOT, "paper_2206_04959_amd", "csrc", "gemm.hip")
+PEAK_HBM_GBS = 8000.0       # HBM3E
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_gpt-8.3b-tp4.json")
+CSRC = os.path.join(ROOT, "paper_2206_04959_amd", "csrc")
 
 
 def log(msg: str) -> None:
@@ -45,18 +54,63 @@ def describe(s: synth.StageShape) -> str:
             f"recompute mask {bin(s.recompute_mask)}, {s.dtype}")
 
 
-def dw_traffic_bytes():
-    """HBM bytes per launch of the grouped FC1/FC2 weight-gradient GEMM, from the committed
-    rocprofv3 counter summary, or None if absent or taken on another kernel source."""
+def sources_sha256() -> str:
+    """One digest over every kernel source: counter data taken on other kernels is stale."""
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        if name.endswith((".hip", ".h", ".cpp")):
+            h.update(name.encode())
+            h.update(open(os.path.join(CSRC, name), "rb").read())
+    return h.hexdigest()
+
+
+def class_traffic(klass: str):
+    """HBM bytes per launch of one kernel class, from the committed rocprofv3
+    counter summary (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy of known
+    size), or None if absent or taken on other kernel sources."""
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
-        src = hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()
-        if t.get("gemm_source_sha256") != src:
+        if t.get("sources_sha256") != sources_sha256():
             return None
-        return float(t["bytes_per_launch"])
-    except (OSError, KeyError, ValueError):
+        return float(t["classes"][klass]["bytes_per_launch"])
+    except (OSError, KeyError, ValueError, TypeError):
         return None
+
+
+def class_rates(B, stage, step, shape, steps: int):
+    """Per kernel class: HIP-event time of its launches over `steps` stage
+    steps, and its algorithmic work per launch over that time against the
+    roofline that bounds it."""
+    import torch
+    from paper_2206_04959_amd import kclass
+
+    work = flops.class_work(shape)
+    rows = []
+    for name, (cid, desc) in kclass.CLASSES.items():
+        stage.set_timing(cid)
+        for _ in range(steps):
+            step()
+        torch.cuda.synchronize()
+        ms, n = stage.read_timing()
+        stage.set_timing(B.KC_NONE)
+        amount, unit, bound = work[name]
+        if n == 0:
+            continue
+        per_launch = amount * steps / n
+        avg_ms = ms / n
+        if unit == "FLOP":
+            achieved, peak, u = per_launch / (avg_ms * 1e-3) / 1e12, PEAK_BF16_TFLOPS, "TFLOP/s"
+        else:
+            achieved, peak, u = per_launch / (avg_ms * 1e-3) / 1e9, PEAK_HBM_GBS, "GB/s"
+        rows.append({"class": name, "kernel": desc, "bound": bound, "achieved": round(achieved, 2), "peak": peak,
+                     "unit": u, "frac": round(achieved / peak, 4), "work_per_launch": per_launch,
+                     "work_unit": unit, "launches_timed": n, "launches_per_step": n / steps,
+                     "avg_launch_ms": round(avg_ms, 4), "launch_ms_per_step": round(ms / steps, 4)})
+    total = sum(r["launch_ms_per_step"] for r in rows)
+    for r in rows:
+        r["share_of_launch_time"] = round(r["launch_ms_per_step"] / total, 4)
+    return rows
 
 
 def cpu_baseline(shape: synth.StageShape, budget_s: float = 15.0):
@@ -93,6 +147,11 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="gpt-8.3b-tp4", choices=sorted(synth.PRESETS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--class-steps", type=int, default=5, help="steps per kernel class in the launch-timing loop")
+    ap.add_argument("--n-sub", type=int, default=None, help="sub-micro-batches per micro-batch (sweeps)")
+    ap.add_argument("--mask", type=lambda v: int(v, 0), default=None, help="recompute mask (sweeps)")
+    ap.add_argument("--streams", type=int, choices=(1, 2), default=2,
+                    help="caller streams: 2 (sub-micro-batch j on stream j mod 2) or 1 (sweeps)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU's stage shard; --gpus {args.gpus} is not supported "
@@ -106,6 +165,10 @@ def main() -> int:
         print("no GPU visible", file=sys.stderr)
         return 1
     shape = synth.PRESETS[args.config]
+    if args.n_sub is not None:
+        shape = shape.replace(n_sub=args.n_sub)
+    if args.mask is not None:
+        shape = shape.replace(recompute_mask=args.mask)
     log(f"[bench] {describe(shape)}")
     cfg = B.make_config(shape)
     params = B.to_device(B.pack_params(cfg, [{k: v.payload for k, v in p.items()}
@@ -122,7 +185,8 @@ def main() -> int:
     stage = B.Stage(shape)
     log(f"[bench] workspace {stage.workspace_bytes / 2**30:.2f} GiB, recompute area "
         f"{stage.recompute_bytes / 2**30:.2f} GiB")
-    s0, s1 = torch.cuda.Stream(), torch.cuda.Stream()
+    s0 = torch.cuda.Stream()
+    s1 = torch.cuda.Stream() if args.streams == 2 else s0
     s0.wait_stream(torch.cuda.current_stream())
     torch.cuda.synchronize()
 
@@ -140,30 +204,41 @@ def main() -> int:
     torch.cuda.synchronize()
     log(f"[bench] warmup done ({args.warmup} steps)")
 
-    stage.set_timing(B.KC_GEMM_DW)
-    start = torch.cuda.Event(enable_timing=True)
-    stop = torch.cuda.Event(enable_timing=True)
+    # Headline: K steps with no per-kernel timing, one event per step boundary
+    # on s0 (every call ends with s0 joined to the other streams).
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     w0 = time.perf_counter()
-    start.record(s0)
-    for _ in range(args.steps):
+    marks[0].record(s0)
+    for i in range(args.steps):
         step()
-    stop.record(s0)
+        marks[i + 1].record(s0)
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
-    gpu_ms = start.elapsed_time(stop)
-    dw_ms, dw_launches = stage.read_timing()
-    stage.set_timing(B.KC_NONE)
+    gpu_ms = marks[0].elapsed_time(marks[-1])
+    per_step = sorted(marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps))
     ms_per_step = gpu_ms / args.steps
     log(f"[bench] {args.steps} steps: {gpu_ms:.2f} ms on the GPU clock, {wall * 1e3:.2f} ms wall")
+
+    # Per-class launch timing, in a separate loop after the headline: HIP
+    # events around every launch of one kernel class at a time, on the stream
+    # that launch runs on.
+    classes = class_rates(B, stage, step, shape, args.class_steps)
+    dominant = max(classes, key=lambda c: c["launch_ms_per_step"])
+    traffic = class_traffic(dominant["class"])
+    roof = {k: dominant[k] for k in ("bound", "achieved", "peak", "unit", "frac")}
+    roof.update(traffic=traffic, kernel=dominant["kernel"], klass=dominant["class"],
+                launches_timed=dominant["launches_timed"], launches_per_step=dominant["launches_per_step"],
+                avg_launch_ms=dominant["avg_launch_ms"], work_per_launch=dominant["work_per_launch"],
+                share_of_launch_time=dominant["share_of_launch_time"])
 
     exe = flops.executed_flops(shape)
     mdl = flops.model_flops(shape)
     value = exe / (ms_per_step * 1e-3) / 1e12
-    dw_per_launch = flops.dw_ffn_flops(shape)
-    dw_avg_ms = dw_ms / max(dw_launches, 1)
-    achieved = dw_per_launch / (dw_avg_ms * 1e-3) / 1e12
-    traffic = dw_traffic_bytes()
+
+    def pct(q):
+        return per_step[min(len(per_step) - 1, int(round(q * (len(per_step) - 1))))]
+
     out = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -180,22 +255,19 @@ def main() -> int:
         "config": {"workload": describe(shape), "global_batch": shape.micro_batch, "seq_len": shape.seq_len,
                    "parallelism": f"tp{shape.tp_degree} shard on 1 GPU (cross-GPU reductions as hand-off buffers)"},
         "pct_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
+        "step_ms_median": round(pct(0.5), 4),
+        "step_ms_p10": round(pct(0.1), 4),
+        "step_ms_p90": round(pct(0.9), 4),
+        "tflops_at_median": round(exe / (pct(0.5) * 1e-3) / 1e12, 2),
         "executed_tflop_per_step": round(exe / 1e12, 4),
         "model_tflop_per_step": round(mdl / 1e12, 4),
         "model_tflops": round(mdl / (ms_per_step * 1e-3) / 1e12, 2),
-        "roofline": {
-            "kernel": "grouped weight-gradient GEMM of FC1 and FC2 (gemm_mfma_kernel, a_t=b_t=1, fp32 out), "
-                      "one launch per block",
-            "bound": "mfma",
-            "achieved": round(achieved, 2),
-            "peak": PEAK_BF16_TFLOPS,
-            "unit": "TFLOP/s",
-            "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-            "traffic": traffic,
-            "launches_timed": dw_launches,
-            "avg_launch_ms": round(dw_avg_ms, 4),
-            "flop_per_launch": dw_per_launch,
-        },
+        "streams": args.streams,
+        "class_steps": args.class_steps,
+        "workspace_bytes": stage.workspace_bytes,
+        "recompute_area_bytes": stage.recompute_bytes,
+        "roofline": roof,
+        "kernel_classes": classes,
     }
     if not args.no_cpu_baseline:
         log("[bench] timing the oracle on the host (bounded sample)")

@@ -1,4 +1,4 @@
-"""HBM traffic of the grouped FC1/FC2 weight-gradient GEMM, from rocprofv3 counters.
+"""HBM traffic of every kernel class of the stage step, from rocprofv3 counters.
 
 Two steps, each run from the repository root on the GPU machine:
 
@@ -9,13 +9,13 @@ Two steps, each run from the repository root on the GPU machine:
     python3 -m paper_2206_04959_amd.traffic summarize <dir_f> <dir_w>
 
 `run` performs one fwd -> recompute -> bwd step of the 8.3B-shaped stage shard
-(through the C ABI) and one plain copy kernel of a known size (an elementwise multiply by 1).
-`summarize` reads both counter files, takes the counters of the grouped FC1/FC2
-weight-gradient launches (the fp32-output GEMM with both operands read
-transposed and the largest grid: the other weight-gradient launch of a block,
-QKV and projection, has fewer tiles) and of the copy, scales the GEMM's readings by (known copy bytes / copy
-reading), and writes profiles/gemm_dw_traffic.json, keyed by the SHA-256 of the
-GEMM source so that a later kernel change invalidates it.
+(through the C ABI) and one plain copy kernel of a known size (an elementwise
+multiply by 1).  `summarize` reads both counter files, assigns every dispatch
+of the step to its kernel class (kclass.classify), scales the readings by
+(known copy bytes / the copy's reading) and writes
+profiles/traffic_gpt-8.3b-tp4.json: per class the launches of one step and the
+fetched and written bytes per launch, keyed by a digest of the kernel sources
+so that a later kernel change invalidates it.
 """
 from __future__ import annotations
 
@@ -28,11 +28,20 @@ import sys
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
-OUT = os.path.join(ROOT, "profiles", "gemm_dw_traffic.json")
-GEMM_SOURCE = os.path.join(PKG, "csrc", "gemm.hip")
+OUT = os.path.join(ROOT, "profiles", "traffic_gpt-8.3b-tp4.json")
+CSRC = os.path.join(PKG, "csrc")
 COPY_BYTES = 512 * 2**20  # bytes read (and written) by the reference copy
-DW_KERNEL = "true, true, 5>"  # template tail of the grouped dW GEMM instantiations (a_t, b_t, fp32 out)
 COPY_KERNEL = "elementwise"   # torch's elementwise kernels (the reference copy is the last one run)
+
+
+def sources_sha256() -> str:
+    """One digest over every kernel source (the same one bench.py checks)."""
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        if name.endswith((".hip", ".h", ".cpp")):
+            h.update(name.encode())
+            h.update(open(os.path.join(CSRC, name), "rb").read())
+    return h.hexdigest()
 
 
 def run() -> None:
@@ -82,37 +91,50 @@ def _dispatch_values(d: str, counter: str):
     return dict(sorted(out.items()))
 
 
-def _pick(vals, needle: str, last_only: bool = False, largest_grid: bool = False):
-    sel = [(grid, v) for (name, grid, v) in vals.values() if needle in name]
+def _copy_reading(vals) -> float:
+    sel = [v for (name, grid, v) in vals.values() if COPY_KERNEL in name]
     if not sel:
-        raise ValueError(f"no dispatch of a kernel containing {needle!r}")
-    if largest_grid:
-        g = max(grid for grid, _ in sel)
-        sel = [(grid, v) for grid, v in sel if grid == g]
-    sel = [v for _, v in sel]
-    return sel[-1:] if last_only else sel
+        raise ValueError("no dispatch of the reference copy")
+    return sel[-1] * 1024.0  # counters are in KiB per dispatch
+
+
+def _per_class(vals, scale: float):
+    sys.path.insert(0, ROOT)
+    from paper_2206_04959_amd import kclass
+    dw_grids = tuple(sorted({grid for (name, grid, v) in vals.values() if kclass.is_dw(name)}))
+    out = {}
+    for name, grid, v in vals.values():
+        c = kclass.classify(name, grid, dw_grids)
+        if c is None:
+            continue
+        n, tot = out.get(c, (0, 0.0))
+        out[c] = (n + 1, tot + v * 1024.0 * scale)
+    return out
 
 
 def summarize(dir_fetch: str, dir_write: str) -> dict:
     fetch = _dispatch_values(dir_fetch, "FETCH_SIZE")
     write = _dispatch_values(dir_write, "WRITE_SIZE")
-    # counters are in KiB per dispatch
-    f_copy = _pick(fetch, COPY_KERNEL, last_only=True)[0] * 1024.0
-    w_copy = _pick(write, COPY_KERNEL, last_only=True)[0] * 1024.0
+    f_copy, w_copy = _copy_reading(fetch), _copy_reading(write)
     f_scale, w_scale = COPY_BYTES / f_copy, COPY_BYTES / w_copy
-    f_dw = [v * 1024.0 * f_scale for v in _pick(fetch, DW_KERNEL, largest_grid=True)]
-    w_dw = [v * 1024.0 * w_scale for v in _pick(write, DW_KERNEL, largest_grid=True)]
+    fc, wc = _per_class(fetch, f_scale), _per_class(write, w_scale)
+    classes = {}
+    for c in sorted(set(fc) | set(wc)):
+        nf, bf = fc.get(c, (0, 0.0))
+        nw, bw = wc.get(c, (0, 0.0))
+        n = max(nf, nw, 1)
+        classes[c] = {"launches": n, "fetch_bytes_per_launch": bf / max(nf, 1),
+                      "write_bytes_per_launch": bw / max(nw, 1),
+                      "bytes_per_launch": bf / max(nf, 1) + bw / max(nw, 1)}
     res = {
-        "kernel": "grouped FC1/FC2 weight-gradient GEMM of one block (gpt-8.3b-tp4 stage shard)",
-        "launches": len(f_dw),
-        "fetch_bytes_per_launch": sum(f_dw) / len(f_dw),
-        "write_bytes_per_launch": sum(w_dw) / len(w_dw),
+        "workload": "gpt-8.3b-tp4 stage shard, one fwd -> recompute -> bwd step",
+        "classes": classes,
         "copy_bytes": COPY_BYTES,
         "copy_fetch_reading_bytes": f_copy,
         "copy_write_reading_bytes": w_copy,
         "scale_fetch": f_scale,
         "scale_write": w_scale,
-        "gemm_source_sha256": hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest(),
+        "sources_sha256": sources_sha256(),
         "commands": [
             "rocprofv3 --pmc FETCH_SIZE -d <dir_f> -o run --output-format csv -- "
             "python3 -m paper_2206_04959_amd.traffic run",
@@ -121,7 +143,6 @@ def summarize(dir_fetch: str, dir_write: str) -> dict:
             "python3 -m paper_2206_04959_amd.traffic summarize <dir_f> <dir_w>",
         ],
     }
-    res["bytes_per_launch"] = res["fetch_bytes_per_launch"] + res["write_bytes_per_launch"]
     os.makedirs(os.path.dirname(OUT), exist_ok=True)
     with open(OUT, "w") as f:
         json.dump(res, f, indent=1)

@@ -1,5 +1,16 @@
 """Helpers for the GPU parity tests: run the HIP stage through the C ABI and the
-oracle on the same seeded inputs, and compare with the max-relative metric."""
+oracle on the same seeded inputs, and compare them.
+
+Metrics, per output tensor:
+* max-relative: max_i |g_i - o_i| / max_i |o_i|, bar 2e-2 in bf16 and 1e-4 in
+  the fp32 check mode (the stated tolerances);
+* elementwise relative with a floor: max_i |g_i - o_i| / max(|o_i|, 1e-3 max|o|),
+  which also sees errors on the small elements of a tensor.  It gates the tiny
+  fp32 workload at ELEM_TOL_FP32 and is reported for the others.  The bar is
+  derived from the arithmetic: the same oracle evaluated entirely in fp32 numpy
+  (unit roundoff 6e-8, length-1024 dot products) stays at or below 4.4e-4 on
+  that workload; the GPU's summation order differs, so the bar leaves about 4x.
+"""
 import numpy as np
 import pytest
 
@@ -21,6 +32,18 @@ def rel_err(got, ref) -> float:
     got = np.asarray(got, dtype=np.float64)
     den = float(np.max(np.abs(ref)))
     return float(np.max(np.abs(got - ref))) / (den if den > 0 else 1.0)
+
+
+ELEM_FLOOR = 1e-3
+ELEM_TOL_FP32 = 2e-3
+
+
+def elem_err(got, ref, floor: float = ELEM_FLOOR) -> float:
+    ref = np.asarray(ref, dtype=np.float64)
+    got = np.asarray(got, dtype=np.float64)
+    big = float(np.max(np.abs(ref)))
+    den = np.maximum(np.abs(ref), floor * (big if big > 0 else 1.0))
+    return float(np.max(np.abs(got - ref) / den))
 
 
 def tol_for(shape) -> float:
@@ -107,15 +130,16 @@ def oracle_results(shape):
     return oracle.shard_run(x, dy, params, shape.local_heads, shape.ln_eps)
 
 
-def compare(got, ref, shape, tol=None, blocks=None):
-    """Return {tensor name: error}; every error must be <= tol."""
+def compare(got, ref, shape, tol=None, blocks=None, metric=rel_err):
+    """Return ({tensor name: error}, {failing ones}); every error must be <= tol.
+    `metric` is rel_err (the max-relative metric) or elem_err."""
     tol = tol_for(shape) if tol is None else tol
-    errs = {"y": rel_err(got["y"], ref["y"]), "dx": rel_err(got["dx"], ref["dx"])}
+    errs = {"y": metric(got["y"], ref["y"]), "dx": metric(got["dx"], ref["dx"])}
     for l in (range(shape.n_blocks) if blocks is None else blocks):
         if "p_o" in got:
             for k in ("p_o", "p_f", "d_ln1", "d_ln2"):
-                errs[f"{k}[{l}]"] = rel_err(got[k][l], ref[k][l])
+                errs[f"{k}[{l}]"] = metric(got[k][l], ref[k][l])
         for name in synth.PARAM_NAMES:
-            errs[f"{name}[{l}]"] = rel_err(got["grads"][l][name], ref["grads"][l][name])
+            errs[f"{name}[{l}]"] = metric(got["grads"][l][name], ref["grads"][l][name])
     bad = {k: v for k, v in errs.items() if not (v <= tol)}
     return errs, bad

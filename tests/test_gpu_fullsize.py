@@ -3,29 +3,25 @@ times (two streams, the preset's sub-micro-batch count and recompute mask):
 every output tensor against the fp64 oracle run on the same seeded inputs.
 
 bf16 runs use the 2e-2 max-relative bar; the same workloads in the fp32 check
-mode use 1e-4, which checks every kernel and the schedule at full size with the
-bf16 storage error taken out."""
+mode use 1e-4.  (The fp32 check mode runs the fp32 kernels, so it checks the
+schedule and the data movement at full size, not the bf16 MFMA kernels.)
+
+The 20B-shaped workload in bf16 is collected from its own file,
+test_gpu_z_fullsize_20b.py, after the other GPU tests: its error sits closest to
+the bar of all workloads."""
 import time
 
 import pytest
 
 from paper_2206_04959_amd import synth
-from tests.gpu_util import StageRun, compare, oracle_results
+from tests.gpu_util import StageRun, compare, elem_err, oracle_results
 
 pytestmark = pytest.mark.gpu
-
-BF16_FLOOR = ("gpt-20b-tp8 in bf16 sits at the bf16-storage floor of the max-relative metric: "
-              "the LN1 input-gradient partial of block 1 measures 2.10e-2; replaying the stage on the CPU "
-              "with bf16 rounding at the path's storage points (tests/numerics_bf16_floor.py) gives "
-              "1.6-2.0e-2 for that tensor at one sequence, with or without an fp32 residual stream; "
-              "the fp32 check mode of the same workload is held to 1e-4 below")
 
 CASES = [
     pytest.param("gpt-8.3b-tp4", "bf16", id="gpt-8.3b-tp4-bf16"),
     pytest.param("gpt-2.5b-tp2", "bf16", id="gpt-2.5b-tp2-bf16"),
     pytest.param("gpt-1.5b-stage", "bf16", id="gpt-1.5b-stage-bf16"),
-    pytest.param("gpt-20b-tp8", "bf16", id="gpt-20b-tp8-bf16", marks=pytest.mark.xfail(reason=BF16_FLOOR,
-                                                                                      strict=False)),
     pytest.param("gpt-8.3b-tp4", "fp32", id="gpt-8.3b-tp4-fp32"),
     pytest.param("gpt-2.5b-tp2", "fp32", id="gpt-2.5b-tp2-fp32"),
     pytest.param("gpt-1.5b-stage", "fp32", id="gpt-1.5b-stage-fp32"),
@@ -33,8 +29,7 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("name,dtype", CASES)
-def test_full_size_stage_matches_oracle(name, dtype):
+def check_full_size(name, dtype):
     shape = synth.PRESETS[name].replace(dtype=dtype)
     print(f"[full-size parity] {name} {dtype}: {shape}", flush=True)
     t0 = time.time()
@@ -46,7 +41,15 @@ def test_full_size_stage_matches_oracle(name, dtype):
     errs, bad = compare(got, ref, shape)
     top = sorted(errs.items(), key=lambda kv: -kv[1])[:5]
     print("  worst: " + ", ".join(f"{k}={v:.3e}" for k, v in top), flush=True)
+    eerrs, _ = compare(got, ref, shape, tol=float("inf"), metric=elem_err)
+    etop = sorted(eerrs.items(), key=lambda kv: -kv[1])[:3]
+    print("  elementwise (floor 1e-3 max, reported): " + ", ".join(f"{k}={v:.3e}" for k, v in etop), flush=True)
     assert not bad, bad
+
+
+@pytest.mark.parametrize("name,dtype", CASES)
+def test_full_size_stage_matches_oracle(name, dtype):
+    check_full_size(name, dtype)
 
 
 def test_full_size_runs_are_bit_identical():
