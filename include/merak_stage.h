@@ -376,6 +376,24 @@ int merak_layernorm_bwd(int dtype, int rows, int h, const void* dout, const void
                         const void* dres, void* dx, float* dgamma, float* dbeta,
                         int accumulate, float* scratch, void* stream);
 
+/* merak_layernorm_bwd without the scratch argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments, kernels and results as
+ * merak_layernorm_bwd (bit for bit).  The partial sums go to a scratch array the
+ * library holds in its own device memory: merak_noalloc_scratch_elems() fp32
+ * elements (16 MiB) per GPU, kept until the process ends; the call allocates
+ * nothing.  Requires 2 * merak_reduce_scratch_elems(rows, h) <=
+ * merak_noalloc_scratch_elems(), else MERAK_ERR_WORKSPACE with nothing
+ * enqueued.  The first call on a device looks up the array's address there
+ * (MERAK_ERR_HIP if that fails).  Every call on one GPU shares that GPU's
+ * array: calls that may overlap on one GPU (other streams, other host threads)
+ * race and must be ordered by the caller. */
+int merak_layernorm_bwd_noalloc(int dtype, int rows, int h, const void* dout, const void* x,
+                                const float* mean, const float* rstd, const void* gamma,
+                                const void* dres, void* dx, float* dgamma, float* dbeta,
+                                int accumulate, void* stream);
+size_t merak_noalloc_scratch_elems(void);
+
 /* out[c] (= or +=) sum over rows r of x[r, c] (fp32 out; cols % 8 == 0), fixed
  * summation order.  scratch: fp32, merak_reduce_scratch_elems(rows, cols). */
 int merak_column_sum(int dtype, int rows, int cols, const void* x, float* out, int accumulate,

@@ -66,6 +66,8 @@ _SIGS = {
     "merak_layernorm_fwd": ([_I, _I, _I, _F, _P, _P, _P, _P, _P, _P, _P], _I),
     "merak_reduce_scratch_elems": ([_I, _I], _SZ),
     "merak_layernorm_bwd": ([_I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _P, _P], _I),
+    "merak_layernorm_bwd_noalloc": ([_I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _P], _I),
+    "merak_noalloc_scratch_elems": ([], _SZ),
     "merak_column_sum": ([_I, _I, _I, _P, _P, _I, _P, _P], _I),
     "merak_attention_fwd": ([_I, _I, _I, _I, _I, _P, _P, _P, _P], _I),
     "merak_attention_bwd": ([_I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P], _I),
@@ -308,6 +310,18 @@ def layernorm_bwd(dout, x, mean, rstd, gamma, dres, dx, dgamma, dbeta, scratch, 
     _check(lib().merak_layernorm_bwd(_dt(x), rows, h, _ptr(dout), _ptr(x), _ptr(mean), _ptr(rstd), _ptr(gamma),
                                      _ptr(dres), _ptr(dx), _ptr(dgamma), _ptr(dbeta), int(accumulate),
                                      _ptr(scratch), _stream(stream)), "merak_layernorm_bwd")
+
+
+def layernorm_bwd_noalloc(dout, x, mean, rstd, gamma, dres, dx, dgamma, dbeta, accumulate=False,
+                          stream=None) -> None:
+    rows, h = x.shape[0], x.shape[-1]
+    _check(lib().merak_layernorm_bwd_noalloc(_dt(x), rows, h, _ptr(dout), _ptr(x), _ptr(mean), _ptr(rstd),
+                                             _ptr(gamma), _ptr(dres), _ptr(dx), _ptr(dgamma), _ptr(dbeta),
+                                             int(accumulate), _stream(stream)), "merak_layernorm_bwd_noalloc")
+
+
+def noalloc_scratch_elems() -> int:
+    return int(lib().merak_noalloc_scratch_elems())
 
 
 def column_sum(x, out, scratch, accumulate=False, stream=None) -> None:

@@ -91,6 +91,13 @@ struct ReduceJob {
 };
 hipError_t launch_reduce_partials_batch(const ReduceJob* jobs, int n, hipStream_t stream);
 
+// Library-owned scratch of the allocation-free LayerNorm backward
+// (merak_layernorm_bwd_noalloc): kNoAllocScratchFloats fp32 elements per GPU.
+// noalloc_scratch returns its device address on the current device, taking it
+// with hipGetSymbolAddress on the first call per device.
+constexpr size_t kNoAllocScratchFloats = (size_t)4 << 20;  // 16 MiB
+hipError_t noalloc_scratch(float** out);
+
 // Causal attention on packed qkv [batch, seq, 3, heads, d].  One launch may
 // cover `members` groups of `batch` sequences each, member m starting
 // m * member_stride sequences after the pointers given (so the sub-micro-

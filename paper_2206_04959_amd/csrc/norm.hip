@@ -10,6 +10,9 @@
 // kReduceRows rows and a 512-column slice, its 4 waves take every 4th row of
 // the segment, and their register sums are added in wave order into one
 // partial row; reduce_partials then adds the partials in segment order.
+#include <atomic>
+#include <mutex>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -385,6 +388,43 @@ hipError_t launch_reduce_partials(int groups, int cols, const float* part, float
                                   hipStream_t stream) {
   const ReduceJob j{groups, cols, part, out, accumulate};
   return launch_reduce_partials_batch(&j, 1, stream);
+}
+
+// ---------------------------------------------------------------------------
+// Scratch of the allocation-free LayerNorm backward: a fixed-size array in the
+// library's own device memory, one copy per GPU, held until the process ends.
+// The host never passes the array's name to a kernel (on the host it stands
+// for a host-side shadow): its device address is taken once per device with
+// hipGetSymbolAddress and kept per device.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) float scratch[kNoAllocScratchFloats];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+std::atomic<float*> g_scratch_ptr[kMaxDevices];
+}  // namespace
+
+hipError_t noalloc_scratch(float** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  float* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+    if (!p) {
+      void* addr = nullptr;
+      e = hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch));
+      if (e != hipSuccess) return e;
+      if (!addr) return hipErrorInvalidSymbol;
+      p = static_cast<float*>(addr);
+      g_scratch_ptr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *out = p;
+  return hipSuccess;
 }
 
 }  // namespace merak

@@ -1045,6 +1045,31 @@ int merak_layernorm_bwd(int dtype, int rows, int h, const void* dout, const void
   return MERAK_OK;
 }
 
+int merak_layernorm_bwd_noalloc(int dtype, int rows, int h, const void* dout, const void* x, const float* mean,
+                                const float* rstd, const void* gamma, const void* dres, void* dx, float* dgamma,
+                                float* dbeta, int accumulate, void* stream) {
+  if (dtype != MERAK_BF16 && dtype != MERAK_FP32) return MERAK_ERR_INVALID_ARG;
+  if (rows <= 0 || h <= 0 || h % 8 || h > 8192) return MERAK_ERR_SHAPE;
+  if (accumulate != 0 && accumulate != 1) return MERAK_ERR_INVALID_ARG;
+  TRY(check_ptr(dout)); TRY(check_ptr(x)); TRY(check_ptr(mean)); TRY(check_ptr(rstd)); TRY(check_ptr(gamma));
+  TRY(check_ptr(dres)); TRY(check_ptr(dx)); TRY(check_ptr(dgamma)); TRY(check_ptr(dbeta));
+  const size_t n = merak_reduce_scratch_elems(rows, h);
+  if (2 * n > kNoAllocScratchFloats) return MERAK_ERR_WORKSPACE;
+  float* scratch = nullptr;  // the library's array on the current device
+  HIP_TRY(noalloc_scratch(&scratch));
+  hipStream_t st = (hipStream_t)stream;
+  const int G = (int)reduce_groups(rows);
+  // Same kernels and order as merak_layernorm_bwd; the partial-sum kernel
+  // writes every scratch element the reduction then reads.
+  HIP_TRY(launch_layernorm_bwd(dtype, rows, h, dout, x, mean, rstd, gamma, dres, dx, st));
+  HIP_TRY(launch_layernorm_param_partials(dtype, rows, h, dout, x, mean, rstd, scratch, scratch + n, st));
+  HIP_TRY(launch_reduce_partials(G, h, scratch, dgamma, accumulate, st));
+  HIP_TRY(launch_reduce_partials(G, h, scratch + n, dbeta, accumulate, st));
+  return MERAK_OK;
+}
+
+size_t merak_noalloc_scratch_elems(void) { return kNoAllocScratchFloats; }
+
 int merak_column_sum(int dtype, int rows, int cols, const void* x, float* out, int accumulate, float* scratch,
                      void* stream) {
   if (dtype != MERAK_BF16 && dtype != MERAK_FP32) return MERAK_ERR_INVALID_ARG;
