@@ -54,4 +54,4 @@ def classify(kernel_name: str, grid: int, dw_grids: tuple = ()) -> str | None:
 
 
 def is_dw(kernel_name: str) -> bool:
-    return "gemm_mfma_kernel" in kernel_name and kernel_name.rstrip("> )").endswith("true, true, 5")
+    return "gemm_mfma_kernel" in kernel_name and "true, true, 5>" in kernel_name
