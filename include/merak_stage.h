@@ -207,6 +207,15 @@ typedef enum {
  * two reads.  Host-side bookkeeping only; results do not change. */
 int merak_stage_set_timing(merak_stage_t stage, int kernel_class);
 
+/* Failure injection for tests of the error paths: after `launches` more kernel
+ * launches by the stage calls (any handle), the next one is not made and its
+ * call returns MERAK_ERR_HIP, as if the launch had failed; -1 turns it off.
+ * Returns the previous setting.  A stage call that fails part-way leaves its
+ * handle refusing the calls that depend on it: a failed fwd leaves the handle
+ * idle, a failed recompute leaves it (and any handle that filled the same
+ * recompute area before) unable to run bwd, a failed bwd leaves it idle. */
+int merak_debug_fail_after(int launches);
+
 /* After the caller has synchronised: total milliseconds of the recorded launches
  * (sum of per-launch event intervals) and their count; then clears the record.
  * MERAK_ERR_ORDER if more than 4096 launches were made since the last read. */
@@ -263,6 +272,30 @@ typedef enum { MERAK_OP_FWD = 0, MERAK_OP_RECOMPUTE = 1, MERAK_OP_BWD = 2, MERAK
  * (at most 3 m).  1 <= n_stages <= 1024, 1 <= n_micro < 2^24, 0 <= stage <
  * n_stages.  MERAK_ERR_WORKSPACE if capacity is too small (*n_ops = needed). */
 int merak_schedule_stage(int kind, int n_stages, int n_micro, int stage, int32_t* ops, int capacity, int* n_ops);
+
+/* Largest number of this stage's micro-batches between their forward and their
+ * backward at any point of its op list (the handles merak_schedule_run needs). */
+int merak_schedule_inflight(int kind, int n_stages, int n_micro, int stage, int* max_inflight);
+
+/* Run stage `stage`'s op list on this GPU: each F, R and B becomes a
+ * merak_stage_fwd, merak_stage_recompute or merak_stage_bwd call (an R+B op
+ * both), on stream0/stream1, in list order.  Micro-batch j reads x[j] and dy[j]
+ * and writes y[j] and dx[j] ([micro_batch, seq_len, hidden] each, as for the
+ * stage calls); the inputs of other stages are the caller's (on one GPU they
+ * are already resident).  A micro-batch takes one of the n_handles handles at
+ * its forward and returns it after its backward, so n_handles must be at least
+ * merak_schedule_inflight(...) (else MERAK_ERR_WORKSPACE); the handles must be
+ * distinct, share one configuration (else MERAK_ERR_SHAPE) and may share one
+ * recompute area when at most one micro-batch is between R and B at a time, as
+ * in these schedules (a taken-over area gives MERAK_ERR_ORDER).  The backwards
+ * add into grads in micro-batch order; the first one overwrites it when
+ * accumulate = 0.  Under MERAK_SCHED_SCP the last stage runs no R, so its
+ * handles need recompute_mask = 0 (else its first backward returns
+ * MERAK_ERR_ORDER).  Arguments are checked before anything is enqueued; an
+ * error returned by a stage call leaves the calls before it enqueued. */
+int merak_schedule_run(int kind, int n_stages, int n_micro, int stage, merak_stage_t* handles, int n_handles,
+                       const void* params, const void* const* x, void* const* y, const void* const* dy,
+                       void* const* dx, float* grads, int accumulate, void* stream0, void* stream1);
 
 /* Greedy in-order execution of all stages' op lists with the given costs
  * (a recompute-in-backward op costs cost_rc + cost_bwd): the makespan and each

@@ -60,6 +60,9 @@ _SIGS = {
     "merak_schedule_stage": ([_I, _I, _I, _I, _P, _I, ctypes.POINTER(_I)], _I),
     "merak_schedule_simulate": ([_I, _I, _I, ctypes.c_double, ctypes.c_double, ctypes.c_double,
                                  ctypes.POINTER(ctypes.c_double), _P], _I),
+    "merak_debug_fail_after": ([_I], _I),
+    "merak_schedule_inflight": ([_I, _I, _I, _I, ctypes.POINTER(_I)], _I),
+    "merak_schedule_run": ([_I, _I, _I, _I, _P, _I, _P, _P, _P, _P, _P, _P, _I, _P, _P], _I),
     "merak_graph_shard": ([_I, _P, _P, _P, _P, _P, _I, _P, _I, _P, ctypes.POINTER(ctypes.c_int32), _P, _P, _I], _I),
     "merak_plan_alpha1": ([_I, ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_double,
                            ctypes.POINTER(ctypes.c_double)], _I),
@@ -269,6 +272,23 @@ def schedule_simulate(kind: int, n_stages: int, n_micro: int, cost_fwd=1.0, cost
     return float(mk.value), list(busy)
 
 
+def schedule_inflight(kind: int, n_stages: int, n_micro: int, stage: int) -> int:
+    """Handles merak_schedule_run needs for this stage (micro-batches in flight)."""
+    n = ctypes.c_int()
+    _check(lib().merak_schedule_inflight(kind, n_stages, n_micro, stage, ctypes.byref(n)), "merak_schedule_inflight")
+    return int(n.value)
+
+
+def schedule_run(kind: int, n_stages: int, n_micro: int, stage: int, stages, params, xs, ys, dys, dxs, grads,
+                 accumulate=False, streams=(None, None)) -> None:
+    """Run one stage's op list through its handles (`stages`: Stage objects)."""
+    hs = (ctypes.c_void_p * len(stages))(*[s.handle.value for s in stages])
+    arr = lambda ts: (ctypes.c_void_p * len(ts))(*[t.data_ptr() for t in ts])  # noqa: E731
+    _check(lib().merak_schedule_run(kind, n_stages, n_micro, stage, hs, len(stages), _ptr(params), arr(xs), arr(ys),
+                                    arr(dys), arr(dxs), _ptr(grads), int(accumulate), _stream(streams[0]),
+                                    _stream(streams[1])), "merak_schedule_run")
+
+
 def plan_recompute(n_stages: int, alpha1: float, blocks_per_stage: int):
     """Stage-aware recomputation plan: ([alpha_i], [recompute mask of stage i])."""
     a = (ctypes.c_double * n_stages)()
@@ -283,6 +303,11 @@ def plan_alpha1(n_stages: int, mem_runtime: float, mem_activation: float, capaci
     _check(lib().merak_plan_alpha1(n_stages, mem_runtime, mem_activation, capacity, step, ctypes.byref(out)),
            "merak_plan_alpha1")
     return float(out.value)
+
+
+def debug_fail_after(launches: int) -> int:
+    """Inject a launch failure after `launches` more stage launches (-1: off)."""
+    return int(lib().merak_debug_fail_after(int(launches)))
 
 
 def gemm_tile_override(cfg: int) -> int:

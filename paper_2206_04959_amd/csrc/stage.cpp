@@ -20,6 +20,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <map>
 #include <mutex>
@@ -251,8 +252,20 @@ char* block_acts(merak_stage* S, int l, int phase) {
 
 // Run `launch` (returns hipError_t); if its kernel class is being timed, record
 // a start/stop event pair around it on `st`.
+// Launches left before an injected failure (< 0: none); merak_debug_fail_after.
+std::atomic<int> g_fail_countdown{-1};
+
+bool injected_failure() {
+  int n = g_fail_countdown.load(std::memory_order_relaxed);
+  while (n >= 0) {
+    if (g_fail_countdown.compare_exchange_weak(n, n - 1, std::memory_order_relaxed)) return n == 0;
+  }
+  return false;
+}
+
 template <typename F>
 int timed(merak_stage* S, int cls, hipStream_t st, F&& launch) {
+  if (injected_failure()) return MERAK_ERR_HIP;  // as if the launch had failed
   const bool on = (S->timed_class == cls && cls != MERAK_KC_NONE);
   if (on && S->t_count >= kMaxTimed) S->t_overflow = true;
   const bool rec = on && S->t_count < kMaxTimed;
@@ -638,6 +651,10 @@ int merak_stage_destroy(merak_stage_t S) {
   return MERAK_OK;
 }
 
+int merak_debug_fail_after(int launches) {
+  return g_fail_countdown.exchange(launches < 0 ? -1 : launches);
+}
+
 int merak_stage_set_timing(merak_stage_t S, int kernel_class) {
   if (!S) return MERAK_ERR_INVALID_ARG;
   if (kernel_class < MERAK_KC_NONE || kernel_class >= MERAK_KC_COUNT) return MERAK_ERR_INVALID_ARG;
@@ -681,8 +698,10 @@ int merak_stage_fwd(merak_stage_t S, const void* params, const void* x, void* y,
   if (fwd_partials && !aligned(fwd_partials, 16)) return MERAK_ERR_ALIGN;
   hipStream_t s0 = (hipStream_t)stream0, s1 = (hipStream_t)stream1;
   const Dims& D = S->D;
+  // Idle until every launch of the pass has been enqueued: a failure part-way
+  // leaves a handle that refuses recompute and bwd.
+  S->state = ST_IDLE;
   S->x0 = x;
-  S->state = ST_FWD;
   TRY(fork(S, s0, s1));
   const size_t th = (size_t)D.T * D.h * D.esz;
   for (int l = 0; l < D.L; ++l) {
@@ -694,6 +713,7 @@ int merak_stage_fwd(merak_stage_t S, const void* params, const void* x, void* y,
     TRY(block_forward(S, params, l, A, xin, yout, po, pf, s0, s1));
   }
   TRY(join(S, s0, s1));
+  S->state = ST_FWD;
   return MERAK_OK;
 }
 
@@ -704,6 +724,14 @@ int merak_stage_recompute(merak_stage_t S, const void* params, void* stream0, vo
   if (S->D.mask == 0) return MERAK_OK;
   hipStream_t s0 = (hipStream_t)stream0, s1 = (hipStream_t)stream1;
   const Dims& D = S->D;
+  // The area is this handle's from the first launch on: a handle that filled
+  // it before can no longer run its backward on it, and if a launch fails
+  // part-way neither can this one (its state stays short of RECOMPUTED).
+  {
+    std::lock_guard<std::mutex> lk(g_mu);
+    g_rc_owner[S->rc] = S;
+  }
+  S->state = ST_FWD;
   TRY(fork(S, s0, s1));
   for (int l = 0; l < D.L; ++l) {
     if (!((D.mask >> l) & 1)) continue;
@@ -715,10 +743,6 @@ int merak_stage_recompute(merak_stage_t S, const void* params, void* stream0, vo
     HIP_TRY(hipEventRecord(S->ev_rc[l][1], s1));
   }
   TRY(join(S, s0, s1));
-  {
-    std::lock_guard<std::mutex> lk(g_mu);
-    g_rc_owner[S->rc] = S;
-  }
   S->state = ST_RECOMPUTED;
   return MERAK_OK;
 }
@@ -743,6 +767,7 @@ int merak_stage_bwd(merak_stage_t S, const void* params, const void* dy, void* d
   const Dims& D = S->D;
   const size_t th = (size_t)D.T * D.h * D.esz;
   const size_t th_al = align_up(th, 256);
+  S->state = ST_IDLE;  // consumed, also if a launch fails part-way
   TRY(fork(S, s0, s1));
   HIP_TRY(hipStreamWaitEvent(S->aux, S->ev_fork, 0));
   for (int l = D.L - 1; l >= 0; --l) {
@@ -800,7 +825,6 @@ int merak_stage_bwd(merak_stage_t S, const void* params, const void* dy, void* d
   HIP_TRY(hipEventRecord(S->ev_aux, S->aux));
   TRY(join(S, s0, s1));
   HIP_TRY(hipStreamWaitEvent(s0, S->ev_aux, 0));
-  S->state = ST_IDLE;
   return MERAK_OK;
 }
 
@@ -984,6 +1008,78 @@ int merak_schedule_simulate(int kind, int n_stages, int n_micro, double cost_fwd
   }
   *makespan = *std::max_element(free_at.begin(), free_at.end());
   for (int i = 0; i < s; ++i) busy[i] = work[i];
+  return MERAK_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Running one stage's schedule on this GPU
+// ---------------------------------------------------------------------------
+int merak_schedule_inflight(int kind, int n_stages, int n_micro, int stage, int* max_inflight) {
+  TRY(check_sched(kind, n_stages, n_micro));
+  if (stage < 0 || stage >= n_stages || !max_inflight) return MERAK_ERR_INVALID_ARG;
+  std::vector<int32_t> v;
+  build_stage_ops(kind, n_stages, n_micro, stage, v);
+  int live = 0, most = 0;
+  for (int32_t op : v) {
+    const int type = op >> 24;
+    if (type == MERAK_OP_FWD) most = std::max(most, ++live);
+    if (type == MERAK_OP_BWD || type == MERAK_OP_RECOMPUTE_BWD) --live;
+  }
+  *max_inflight = most;
+  return MERAK_OK;
+}
+
+int merak_schedule_run(int kind, int n_stages, int n_micro, int stage, merak_stage_t* handles, int n_handles,
+                       const void* params, const void* const* x, void* const* y, const void* const* dy,
+                       void* const* dx, float* grads, int accumulate, void* stream0, void* stream1) {
+  TRY(check_sched(kind, n_stages, n_micro));
+  if (stage < 0 || stage >= n_stages || !handles || n_handles < 1 || !x || !y || !dy || !dx)
+    return MERAK_ERR_INVALID_ARG;
+  if (accumulate != 0 && accumulate != 1) return MERAK_ERR_INVALID_ARG;
+  TRY(check_ptr(params));
+  TRY(check_ptr(grads));
+  for (int i = 0; i < n_handles; ++i) {
+    if (!handles[i]) return MERAK_ERR_INVALID_ARG;
+    for (int k = 0; k < i; ++k)
+      if (handles[k] == handles[i]) return MERAK_ERR_INVALID_ARG;
+    if (memcmp(&handles[i]->cfg, &handles[0]->cfg, sizeof(merak_stage_config)) != 0) return MERAK_ERR_SHAPE;
+  }
+  for (int j = 0; j < n_micro; ++j) {
+    TRY(check_ptr(x[j]));
+    TRY(check_ptr(y[j]));
+    TRY(check_ptr(dy[j]));
+    TRY(check_ptr(dx[j]));
+  }
+  int need = 0;
+  TRY(merak_schedule_inflight(kind, n_stages, n_micro, stage, &need));
+  if (n_handles < need) return MERAK_ERR_WORKSPACE;
+  std::vector<int32_t> ops;
+  build_stage_ops(kind, n_stages, n_micro, stage, ops);
+  // One handle per micro-batch in flight: taken at its forward, returned after
+  // its backward.  Every call goes to the same two streams in op order, so the
+  // gradients accumulate in backward order (micro-batch 0 first).
+  std::vector<int> free_list, owner(n_micro, -1);
+  for (int i = n_handles - 1; i >= 0; --i) free_list.push_back(i);
+  int acc = accumulate;
+  for (int32_t op : ops) {
+    const int type = op >> 24, j = op & 0xffffff;
+    if (type == MERAK_OP_FWD) {
+      if (free_list.empty()) return MERAK_ERR_WORKSPACE;  // cannot happen after the count above
+      owner[j] = free_list.back();
+      free_list.pop_back();
+      TRY(merak_stage_fwd(handles[owner[j]], params, x[j], y[j], nullptr, stream0, stream1));
+      continue;
+    }
+    if (owner[j] < 0) return MERAK_ERR_ORDER;
+    merak_stage_t h = handles[owner[j]];
+    if (type == MERAK_OP_RECOMPUTE || type == MERAK_OP_RECOMPUTE_BWD) TRY(merak_stage_recompute(h, params, stream0, stream1));
+    if (type == MERAK_OP_BWD || type == MERAK_OP_RECOMPUTE_BWD) {
+      TRY(merak_stage_bwd(h, params, dy[j], dx[j], grads, acc, nullptr, stream0, stream1));
+      acc = 1;
+      free_list.push_back(owner[j]);
+      owner[j] = -1;
+    }
+  }
   return MERAK_OK;
 }
 

@@ -140,3 +140,50 @@ def test_call_order_errors():
         st.bwd(r.params, r.dy, r.dx, r.grads)
     assert e.value.status == -3
     other.close()
+
+
+def test_failed_launch_leaves_handle_refusing_dependent_calls():
+    """An injected launch failure (merak_debug_fail_after: the call returns
+    MERAK_ERR_HIP instead of making the launch) part-way through fwd, recompute
+    or bwd leaves the handle refusing the calls that would read what the failed
+    call did not finish; after clearing the injection the handle works and
+    gives the same bits as a handle that never failed."""
+    torch = need_gpu()
+    shape = SMALL["d64-t2-bf16"].replace(recompute_mask=0b011)
+    ref = StageRun(shape).run().raw()
+    r = StageRun(shape)
+    st = r.stage
+    try:
+        B.debug_fail_after(3)
+        with pytest.raises(B.MerakError) as e:
+            st.fwd(r.params, r.x, r.y)
+        assert e.value.status == -6
+        B.debug_fail_after(-1)
+        for call in (lambda: st.recompute(r.params), lambda: st.bwd(r.params, r.dy, r.dx, r.grads)):
+            with pytest.raises(B.MerakError) as e:
+                call()
+            assert e.value.status == -3
+        st.fwd(r.params, r.x, r.y)
+        B.debug_fail_after(2)
+        with pytest.raises(B.MerakError) as e:
+            st.recompute(r.params)
+        assert e.value.status == -6
+        B.debug_fail_after(-1)
+        with pytest.raises(B.MerakError) as e:  # recomputation incomplete
+            st.bwd(r.params, r.dy, r.dx, r.grads)
+        assert e.value.status == -3
+        st.recompute(r.params)
+        B.debug_fail_after(5)
+        with pytest.raises(B.MerakError) as e:
+            st.bwd(r.params, r.dy, r.dx, r.grads)
+        assert e.value.status == -6
+        B.debug_fail_after(-1)
+        with pytest.raises(B.MerakError) as e:  # consumed by the failed call
+            st.bwd(r.params, r.dy, r.dx, r.grads)
+        assert e.value.status == -3
+    finally:
+        B.debug_fail_after(-1)
+    torch.cuda.synchronize()
+    got = r.run().raw()
+    for k in ref:
+        assert np.array_equal(ref[k], got[k]), k

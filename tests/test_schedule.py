@@ -110,3 +110,20 @@ def test_abi_schedule_errors():
     assert L.merak_schedule_stage(0, 0, 4, 0, buf, 4, ctypes.byref(n)) == -2
     assert L.merak_schedule_stage(0, 4, 4, 4, buf, 4, ctypes.byref(n)) == -1
     assert L.merak_schedule_stage(0, 4, 4, 0, buf, 4, ctypes.byref(n)) == -5 and n.value == 8
+
+
+@pytest.mark.parametrize("kind", sorted(KINDS))
+def test_abi_inflight_matches_oracle(kind):
+    """The handles merak_schedule_run needs: the peak of micro-batches between
+    their forward and their backward in the oracle's op list."""
+    for s in (1, 2, 3, 4, 8):
+        for m in range(1, 3 * s + 2):
+            for i in range(s):
+                live, peak = 0, 0
+                for op, j in S.stage_ops(kind, s, m, i):
+                    if op == "F":
+                        live += 1
+                        peak = max(peak, live)
+                    elif op in ("B", "RB"):
+                        live -= 1
+                assert B.schedule_inflight(KINDS[kind], s, m, i) == peak, (s, m, i)
