@@ -1,105 +1,124 @@
-"""Plain oracle of the graph-sharding algorithm (Sec. 4.2, Alg. 1 and Alg. 2).
+"""Plain oracle of the graph-sharding algorithm (Sec. 4.2).
 
 TEST INFRASTRUCTURE ONLY (like the rest of this package): used by the tests,
 never by the library.  It shares no code with the C implementation.
 
-The model graph is a DAG whose nodes are visited in topological order.  Each
-node is placed in a subgraph next to its farthest dependency (Alg. 1); a
-subgraph is closed once the parameters it holds exceed sum(params) / k, and its
-output is the node that closed it plus every visited "common" node that still
-has users (Alg. 2).  The result is a sequence of subgraphs that can run one
-after the other, each taking the previous one's outputs and the graph inputs
-it is the first to use.
+What the section states, and what this oracle computes:
+  * the model graph is a DAG; its nodes are visited once, in topological order,
+    while subgraph ids are handed out from 0;
+  * a node must share a subgraph with its farthest dependency.  Its arguments
+    can tie it to: a graph input (the node goes where that input's first reader
+    went), an output of an earlier subgraph (the node may sit in the subgraph
+    right after its producer), or any other node visited before it except the
+    one visited just before (the node goes where that node is).  Common nodes
+    (nodes used by many blocks, such as the attention mask) tie nothing; their
+    remaining uses are counted down instead;
+  * when that dependency lies in an earlier subgraph than the current one, the
+    current subgraph becomes that one, and every node visited after the
+    dependency moves into it;
+  * a subgraph closes as soon as the parameters of its nodes exceed the total
+    over the number of subgraphs asked for; what it hands on is every visited
+    common node that still has uses, then the node that closed it;
+  * each subgraph's inputs are what the one before it handed on, plus the graph
+    inputs it reads first, so the subgraphs run one after the other.
 
-Notation follows the paper: C common node -> remaining user count, X graph
-inputs, I graph input -> first user, M node -> subgraph id, S_outs subgraph id
--> outputs, N visited nodes, D node -> parameter count, p the threshold.
-
-Readings where the listings are silent or ambiguous:
-  * graph inputs are not visited as nodes: they are the set X; a node that
-    reads the same graph input twice is its first user, not a dependency of
-    itself;
-  * when a node's farthest dependency lies in an older subgraph, the nodes
-    visited after that dependency move into its subgraph.  The dependency node
-    itself keeps its subgraph: the listing assigns it too, which only matters
-    when the dependency is the output of an earlier subgraph and would move an
-    output out of the subgraph that produces it;
-  * reopening subgraph s by such a merge discards the outputs recorded for s
-    and every later subgraph: those subgraphs no longer exist, and s records
-    its outputs again when it closes;
-  * the last subgraph is emitted even if it never exceeded the threshold, and
+Readings where the section is silent or ambiguous:
+  * graph inputs are not visited as nodes; a node that reads the same graph
+    input twice is its first reader, not a dependency of itself;
+  * the dependency node itself keeps its subgraph when later nodes move into
+    its subgraph (moving it would take an output out of the subgraph that
+    produces it);
+  * moving nodes back into subgraph s reopens s: the outputs recorded for s and
+    every later subgraph are dropped, and s records its outputs again when it
+    closes;
+  * the last subgraph is emitted even if it never reached the threshold, and
     its outputs are the graph outputs;
-  * a subgraph's inputs are the previous subgraph's outputs plus the graph
-    inputs whose first user it holds (in graph-input order);
-  * the outputs recorded when a subgraph closes list the common nodes in visit
-    order, then the closing node.
+  * the graph inputs of a subgraph are listed in graph-input order, its handed-
+    on common nodes in visit order, then the closing node.
 """
 from __future__ import annotations
 
-from typing import Dict, List, Sequence, Tuple
+from typing import Dict, List, Optional, Sequence, Tuple
 
 
-def search_dependency(n, args, s, C, X, I, M, S_outs, N):
-    """Alg. 1: the smallest subgraph id node n may join and the node that
-    forces it (None if n may stay in subgraph s)."""
-    s_min, n_min = s, None
-    outputs = {o for outs in S_outs.values() for o in outs}
-    for arg in args:
-        if arg in C:  # a common node: no dependency, one user fewer
-            C[arg] -= 1
-        elif arg in X:  # a graph input: stay with its first user
-            if I.get(arg) is None:
-                I[arg] = n
-            elif I[arg] != n and M[I[arg]] < s_min:  # (n reading it twice is no dependency)
-                s_min, n_min = M[I[arg]], I[arg]
-        elif arg in outputs:  # an output of a previous subgraph
-            if M[arg] + 1 < s_min:
-                s_min, n_min = M[arg] + 1, arg
-        elif arg in M and arg != N[-1]:  # another visited node, not the last one
-            if M[arg] < s_min:
-                s_min, n_min = M[arg], arg
-    return s_min, n_min
+class _Walk:
+    """State of one pass over the graph."""
+
+    def __init__(self, graph_inputs: Sequence[str], params: Dict[str, int], common: Dict[str, int], k: int):
+        self.graph_inputs = set(graph_inputs)
+        self.params = params
+        self.uses_left = dict(common)          # common node -> uses not yet visited
+        self.first_reader: Dict[str, str] = {}  # graph input -> first node reading it
+        self.place: Dict[str, int] = {}        # visited node -> subgraph id
+        self.order: List[str] = []             # visited nodes, in visit order
+        self.handed_on: Dict[int, List[str]] = {}  # closed subgraph -> what it hands on
+        self.limit = sum(params.values()) / k
+        self.current = 0
+
+    def _tie(self, node: str, arg: str) -> Optional[Tuple[int, str]]:
+        """(subgraph the argument ties `node` to, the node responsible), or None."""
+        if arg in self.uses_left:
+            self.uses_left[arg] -= 1
+            return None
+        if arg in self.graph_inputs:
+            reader = self.first_reader.setdefault(arg, node)
+            return None if reader == node else (self.place[reader], reader)
+        if any(arg in outs for outs in self.handed_on.values()):
+            return self.place[arg] + 1, arg
+        if arg in self.place and arg != self.order[-1]:
+            return self.place[arg], arg
+        return None
+
+    def farthest_dependency(self, node: str, args: Sequence[str]) -> Tuple[int, Optional[str]]:
+        best, anchor = self.current, None
+        for arg in args:
+            t = self._tie(node, arg)
+            if t is not None and t[0] < best:
+                best, anchor = t
+        return best, anchor
+
+    def pull_back(self, target: int, anchor: str) -> None:
+        """Nodes visited after `anchor` join subgraph `target`, which reopens."""
+        for name in self.order[self.order.index(anchor) + 1:]:
+            self.place[name] = target
+        for sub in [t for t in self.handed_on if t >= target]:
+            del self.handed_on[sub]
+        self.current = target
+
+    def visit(self, node: str, args: Sequence[str]) -> None:
+        target, anchor = self.farthest_dependency(node, args)
+        if target < self.current:
+            self.pull_back(target, anchor)
+        self.place[node] = self.current
+        self.order.append(node)
+        held = sum(self.params.get(m, 0) for m, sub in self.place.items() if sub == self.current)
+        if held > self.limit:
+            live_common = [c for c in self.uses_left if c in self.place and self.uses_left[c] > 0]
+            self.handed_on[self.current] = live_common + [node]
+            self.current += 1
 
 
 def graph_shard(nodes: Sequence[Tuple[str, Sequence[str]]], X: Sequence[str], graph_outputs: Sequence[str],
                 k: int, D: Dict[str, int], C: Dict[str, int]):
-    """Alg. 2.  nodes: (name, argument names) in topological order, graph
-    inputs excluded.  Returns (M, subgraphs) with subgraphs a list of dicts
-    {"nodes", "inputs", "outputs"} in execution order."""
-    C = dict(C)
-    X_order = list(X)
-    X = set(X)
-    M: Dict[str, int] = {}
-    I: Dict[str, str] = {}
-    S_outs: Dict[int, List[str]] = {}
-    N: List[str] = []
-    p = sum(D.values()) / k
-    s = 0
-    for n, args in nodes:
-        s_min, n_min = search_dependency(n, args, s, C, X, I, M, S_outs, N)
-        if s_min < s:
-            s = s_min
-            for n_prev in reversed(N):  # nodes after n_min join its subgraph
-                if n_prev == n_min:
-                    break
-                M[n_prev] = s_min
-            for t in [t for t in S_outs if t >= s_min]:  # subgraph s_min is open again
-                del S_outs[t]
-        M[n] = s
-        N.append(n)
-        p_s = sum(D.get(m, 0) for m in M if M[m] == s)
-        if p_s > p:
-            S_outs[s] = [n_c for n_c in C if n_c in M and C[n_c] > 0]
-            S_outs[s].append(n)
-            s += 1
-    last = max(M.values()) if M else -1
+    """nodes: (name, argument names) in topological order, graph inputs
+    excluded; X: graph inputs; D: parameters per node; C: common nodes with
+    their use counts; k: subgraphs asked for.  Returns (node -> subgraph id,
+    subgraphs), the subgraphs a list of dicts {"nodes", "inputs", "outputs"} in
+    execution order."""
+    walk = _Walk(X, D, C, k)
+    for name, args in nodes:
+        walk.visit(name, args)
+    n_sub = max(walk.place.values()) + 1 if walk.place else 0
     subgraphs = []
-    for s_i in range(last + 1):
-        g_nodes = [n for n, _ in nodes if M[n] == s_i]
-        g_inputs = list(S_outs.get(s_i - 1, [])) + [x for x in X_order if I.get(x) in g_nodes]
-        g_outputs = list(S_outs[s_i]) if s_i < last else list(graph_outputs)
-        subgraphs.append({"nodes": g_nodes, "inputs": g_inputs, "outputs": g_outputs})
-    return M, subgraphs
+    for sub in range(n_sub):
+        members = [name for name, _ in nodes if walk.place[name] == sub]
+        reads_first = [x for x in X if walk.first_reader.get(x) in members]
+        subgraphs.append({
+            "nodes": members,
+            "inputs": list(walk.handed_on.get(sub - 1, [])) + reads_first,
+            "outputs": list(walk.handed_on[sub]) if sub < n_sub - 1 else list(graph_outputs),
+        })
+    return dict(walk.place), subgraphs
 
 
 def from_fx(gm, common_min_users: int = 2):
