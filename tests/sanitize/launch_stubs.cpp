@@ -1,0 +1,26 @@
+// Stand-ins for the kernel launchers (defined in the .hip sources) so that the
+// host sources link without device code.  The host checks never reach them.
+#include <stdlib.h>
+
+#include "kernels.h"
+
+namespace merak {
+static hipError_t unreachable() { abort(); }
+hipError_t launch_gemm(int, bool, bool, int, const GemmProblem*, int, hipStream_t) { return unreachable(); }
+hipError_t launch_layernorm_fwd(int, int, int, float, const void*, const void*, const void*, void*, float*, float*,
+                                hipStream_t, int, int) { return unreachable(); }
+hipError_t launch_layernorm_bwd(int, int, int, const void*, const void*, const float*, const float*, const void*,
+                                const void*, void*, hipStream_t, int, int) { return unreachable(); }
+hipError_t launch_layernorm_param_partials(int, int, int, const void*, const void*, const float*, const float*,
+                                           float*, float*, hipStream_t) { return unreachable(); }
+hipError_t launch_column_partials(int, int, int, const void*, float*, hipStream_t) { return unreachable(); }
+hipError_t launch_reduce_partials(int, int, const float*, float*, int, hipStream_t) { return unreachable(); }
+hipError_t launch_column_partials_batch(int, const ColPartialJob*, int, hipStream_t) { return unreachable(); }
+hipError_t launch_reduce_partials_batch(const ReduceJob*, int, hipStream_t) { return unreachable(); }
+hipError_t noalloc_scratch(float**) { return unreachable(); }
+hipError_t launch_attention_fwd(int, int, int, int, int, const void*, void*, float*, hipStream_t, int, int) {
+  return unreachable();
+}
+hipError_t launch_attention_bwd(int, int, int, int, int, const void*, const void*, const float*, const void*, void*,
+                                float*, hipStream_t, int, int) { return unreachable(); }
+}  // namespace merak
