@@ -368,10 +368,10 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_mfma_kernel(GemmBatch batch
   // ks + 1 are read while the MFMAs of sub-step ks run (two register sets).
   // The one barrier per K stage sits before the last sub-step: by then every
   // wave has read all fragments of stage kt, so the loads of stage kt + NS may
-  // overwrite it, and the first fragments of stage kt + 1 are read while the
+  // overwrite it (issued during that last sub-step and the first sub-step of
+  // stage kt + 1), and the first fragments of stage kt + 1 are read while the
   // last MFMAs of stage kt run.  Before the barrier each wave waits only for
-  // its own loads of stage kt + 1 (later stages stay in flight).  Scheduling
-  // fences keep each sub-step's reads ahead of its MFMAs.
+  // its own loads of stage kt + 1 (later stages stay in flight).
   constexpr int LPT = TileLoader<A_T, BM, NW>::kInst + TileLoader<B_T, BN, NW>::kInst;  // loads per stage
   const int KT = p.K / kBK;
   bf16x8_t a0[TM], a1[TM], b0[TN], b1[TN];  // two fragment register sets
@@ -393,14 +393,60 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_mfma_kernel(GemmBatch batch
     la.issue(ra, st, wave);
     lb.issue(rb, st + A_BYTES, wave);
   };
-  // reads of (st, ks) into set n, then the MFMAs of set c
+  // Instruction order within a sub-step.  The fragment reads of the next
+  // sub-step do not feed the MFMAs of this one, so they are spread between
+  // them (MFMA, read, MFMA, read, ...) rather than issued as one burst ahead
+  // of the MFMAs: a burst of LDS reads from every wave of the workgroup at
+  // once holds up the waves' MFMA issue.  The same holds for the global ->
+  // LDS loads of a later stage, which go out one after each MFMA, split over
+  // two sub-steps (step_loads).  Each such placement is pinned with
+  // scheduling fences, in one code path for the loop body: a second path (a
+  // variant of the sub-step without loads for the last stages) made the
+  // compiler rename the accumulators between the paths and spill.
+  constexpr int NRD = TM * FragReader<A_T, BM>::kInstPerFrag + TN * FragReader<B_T, BN>::kInstPerFrag;
+  constexpr int NMF = TM * TN;
+  constexpr int NIL = NRD > NMF ? NRD : NMF;
+  constexpr int LA = TileLoader<A_T, BM, NW>::kInst;
+  // reads of (st, ks) into set n, interleaved with the MFMAs of set c
   auto step = [&](const char* st, int ks, bf16x8_t (&na)[TM], bf16x8_t (&nb)[TN], const bf16x8_t (&ca)[TM],
                   const bf16x8_t (&cb)[TN]) {
     read_frags(st, ks, na, nb);
-    __builtin_amdgcn_sched_barrier(0);
     mfmas(ca, cb);
+#pragma unroll
+    for (int i = 0; i < NIL; ++i) {
+      if (i < NMF) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+      if (i < NRD) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+    }
     __builtin_amdgcn_sched_barrier(0);
   };
+  // The MFMAs of set c, each followed by global -> LDS load q (q in [Q0, Q1)
+  // of the stage held in LDS buffer `stage`, if do_loads), then the reads of
+  // (st, ks) into set n.
+  auto step_loads = [&](const char* st, int ks, bf16x8_t (&na)[TM], bf16x8_t (&nb)[TN], const bf16x8_t (&ca)[TM],
+                        const bf16x8_t (&cb)[TN], int stage, bool do_loads, auto q0c, auto q1c) {
+    constexpr int Q0 = decltype(q0c)::value, Q1 = decltype(q1c)::value;
+    constexpr int NML = NMF > Q1 - Q0 ? NMF : Q1 - Q0;
+    char* ld = smem + stage * STAGE;
+#pragma unroll
+    for (int u = 0; u < NML; ++u) {
+      if (u < NMF)
+        acc[u / TM][u % TM] =
+            __builtin_amdgcn_mfma_f32_32x32x16_bf16(cb[u / TM], ca[u % TM], acc[u / TM][u % TM], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      const int q = Q0 + u;
+      if (q < Q1) {
+        if (q < LA) {
+          if (do_loads) la.issue_one(ra, ld, wave, q);
+        } else {
+          if (do_loads) lb.issue_one(rb, ld + A_BYTES, wave, q - LA);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    read_frags(st, ks, na, nb);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  constexpr int LH = (LPT + 1) / 2;  // loads of a stage issued right after the barrier; the rest a sub-step later
 
 #pragma unroll
   for (int s = 0; s < NS; ++s)
@@ -414,13 +460,15 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_mfma_kernel(GemmBatch batch
   for (int kt = 0; kt < KT - 1; ++kt) {
     const int cur = kt % NS;
     const char* st = smem + cur * STAGE;
-    step(st, 1, a1, b1, a0, b0);
+    // the second part of the loads of stage kt - 1 + NS, into the buffer stage kt - 1 used
+    step_loads(st, 1, a1, b1, a0, b0, (kt + NS - 1) % NS, kt >= 1 && kt - 1 + NS < KT,
+               std::integral_constant<int, LH>{}, std::integral_constant<int, LPT>{});
     step(st, 2, a0, b0, a1, b1);
     step(st, 3, a1, b1, a0, b0);
     if (kt + NS - 1 < KT) wait_vm_barrier<(NS - 2) * LPT>();
     else wait_vm_barrier<0>();
-    if (kt + NS < KT) issue(cur);
-    step(smem + ((kt + 1) % NS) * STAGE, 0, a0, b0, a1, b1);
+    step_loads(smem + ((kt + 1) % NS) * STAGE, 0, a0, b0, a1, b1, cur, kt + NS < KT,
+               std::integral_constant<int, 0>{}, std::integral_constant<int, LH>{});
   }
   // Epilogues that read a [M, N] operand fetch this lane's chunks of it for
   // the first 32-row slab (in the row-contiguous layout of the staged epilogue
