@@ -29,6 +29,7 @@
 #include <math.h>
 
 #include <atomic>
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
@@ -418,7 +419,8 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_bf16(int S, int H, int Bm, 
     if (2 * it + (wave & 1) < n_qb) {
       tl.issue(smem + (stage * 4 + wave) * TB, lsrc + (size_t)blk * 64 * lgs);
       float* v = vecs + stage * 256 + (wave & 1) * 64 + (is_do ? 128 : 0);
-      wave_vec_load(reinterpret_cast<char*>(v), vsrc + (size_t)blk * 64, lane);
+      if (is_do) wave_vec_load(reinterpret_cast<char*>(v), vsrc + (size_t)blk * 64, lane);
+      else v[lane] = vsrc[(size_t)blk * 64 + lane] * kLog2e;  // lse staged in log2 units
     }
   };
 
@@ -458,7 +460,7 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_bf16(int S, int H, int Bm, 
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int qi = t * 32 + (r >> 2) * 8 + hf * 4 + (r & 3);
-        float pv = __builtin_amdgcn_exp2f(p[r] * scale_log2 - lse_s[qi] * kLog2e);
+        float pv = __builtin_amdgcn_exp2f(fmaf(p[r], scale_log2, -lse_s[qi]));
         if (diag && key > qs + qi) pv = 0.0f;
         p[r] = pv;
         dp[r] = pv * (dp[r] - del_s[qi]);
@@ -611,16 +613,21 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_bf16(int S, int H, int Bm, in
                                                         dp[t], 0, 0, 0);
       }
     }
-    const bool diag = k0 + 63 > q0;
+    // the causal mask only on a block that reaches past the wave's first query
+    auto probs = [&](auto diag_c) {
+      constexpr bool DIAG = decltype(diag_c)::value;
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+      for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int kk = k0 + t * 32 + (r >> 2) * 8 + hf * 4 + (r & 3);
-        float pv = __builtin_amdgcn_exp2f(p[t][r] * scale_log2 - lse2);
-        if (diag && kk > q) pv = 0.0f;
-        dp[t][r] = pv * (dp[t][r] - del);
-      }
+        for (int r = 0; r < 16; ++r) {
+          const int kk = k0 + t * 32 + (r >> 2) * 8 + hf * 4 + (r & 3);
+          float pv = __builtin_amdgcn_exp2f(fmaf(p[t][r], scale_log2, -lse2));
+          if (DIAG && kk > q) pv = 0.0f;
+          dp[t][r] = pv * (dp[t][r] - del);
+        }
+    };
+    if (k0 + 63 > q0) probs(std::true_type{});
+    else probs(std::false_type{});
     bf16x8_t sb[4];
 #pragma unroll
     for (int g = 0; g < 4; ++g) sb[g] = cvt8(dp[g >> 1], (g & 1) * 8);
