@@ -445,11 +445,13 @@ int block_backward_step(merak_stage* S, const void* params, int l, int j, int k,
 }
 
 // Weight, bias and LayerNorm gradients of block l over the whole micro-batch,
-// on stream st, in three parts that can start as soon as the chain has made
+// on stream st, in four parts that can start as soon as the chain has made
 // their inputs: part 0 (dW2, dW1, db2, db1) needs dy and du, i.e. the FC2
-// backward of every sub-micro-batch; part 1 (dW_o, dW_qkv) needs dx1 and dqkv,
-// i.e. the attention backward; part 2 (b_o, b_qkv and both LayerNorms' sums)
-// needs d_ln1, made by the QKV backward.
+// backward of every sub-micro-batch; part 1 (dW_o, dW_qkv) and part 2 (b_o,
+// b_qkv and LayerNorm 2's sums) need dx1, d_ln2 and dqkv, i.e. the attention
+// backward; part 3 (LayerNorm 1's sums) needs d_ln1, made by the QKV
+// backward.  (Splitting parts 2 and 3 leaves only LayerNorm 1's sums after
+// the last block's chain.)
 int block_param_grads(merak_stage* S, int l, int group, const char* A, const char* x, const char* dy, const char* B,
                       const char* d_ln1, const char* d_ln2, float* grads, int acc, hipStream_t st) {
   const Dims& D = S->D;
@@ -484,21 +486,27 @@ int block_param_grads(merak_stage* S, int l, int group, const char* A, const cha
     LAUNCH(MERAK_KC_GEMM_DW_ATTN, st, launch_gemm(dt, true, true, EPI_F32, p, 2, st));
     return MERAK_OK;
   }
-  // QKV and projection biases, both LayerNorms' parameters
-  const ColPartialJob cj[4] = {
-      {0, T, 3 * D.hl, B + Bl.dqkv, nullptr, nullptr, nullptr, part(Bl.p_bqkv), nullptr},
-      {0, T, D.h, B + Bl.dx1, nullptr, nullptr, nullptr, part(Bl.p_bo), nullptr},
-      {1, T, D.h, d_ln2, A + L.x1, (const float*)(A + L.mu2), (const float*)(A + L.rs2), part(Bl.p_g2),
-       part(Bl.p_be2)},
+  if (group == 2) {  // QKV and projection biases, LayerNorm 2's parameters
+    const ColPartialJob cj[3] = {
+        {0, T, 3 * D.hl, B + Bl.dqkv, nullptr, nullptr, nullptr, part(Bl.p_bqkv), nullptr},
+        {0, T, D.h, B + Bl.dx1, nullptr, nullptr, nullptr, part(Bl.p_bo), nullptr},
+        {1, T, D.h, d_ln2, A + L.x1, (const float*)(A + L.mu2), (const float*)(A + L.rs2), part(Bl.p_g2),
+         part(Bl.p_be2)}};
+    LAUNCH(MERAK_KC_REDUCE, st, launch_column_partials_batch(dt, cj, 3, st));
+    const ReduceJob rj[4] = {{G, 3 * D.hl, part(Bl.p_bqkv), g + S->p_off[P_BQKV], acc},
+                             {G, D.h, part(Bl.p_bo), g + S->p_off[P_BO], acc},
+                             {G, D.h, part(Bl.p_g2), g + S->p_off[P_LN2G], acc},
+                             {G, D.h, part(Bl.p_be2), g + S->p_off[P_LN2B], acc}};
+    LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials_batch(rj, 4, st));
+    return MERAK_OK;
+  }
+  // LayerNorm 1's parameters
+  const ColPartialJob cj[1] = {
       {1, T, D.h, d_ln1, x, (const float*)(A + L.mu1), (const float*)(A + L.rs1), part(Bl.p_g1), part(Bl.p_be1)}};
-  LAUNCH(MERAK_KC_REDUCE, st, launch_column_partials_batch(dt, cj, 4, st));
-  const ReduceJob rj[6] = {{G, 3 * D.hl, part(Bl.p_bqkv), g + S->p_off[P_BQKV], acc},
-                           {G, D.h, part(Bl.p_bo), g + S->p_off[P_BO], acc},
-                           {G, D.h, part(Bl.p_g2), g + S->p_off[P_LN2G], acc},
-                           {G, D.h, part(Bl.p_be2), g + S->p_off[P_LN2B], acc},
-                           {G, D.h, part(Bl.p_g1), g + S->p_off[P_LN1G], acc},
+  LAUNCH(MERAK_KC_REDUCE, st, launch_column_partials_batch(dt, cj, 1, st));
+  const ReduceJob rj[2] = {{G, D.h, part(Bl.p_g1), g + S->p_off[P_LN1G], acc},
                            {G, D.h, part(Bl.p_be1), g + S->p_off[P_LN1B], acc}};
-  LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials_batch(rj, 6, st));
+  LAUNCH(MERAK_KC_REDUCE, st, launch_reduce_partials_batch(rj, 2, st));
   return MERAK_OK;
 }
 
@@ -811,13 +819,14 @@ int merak_stage_bwd(merak_stage_t S, const void* params, const void* dy, void* d
       }
       // Parameter gradients on the internal stream once every sub-micro-
       // batch has passed the step that makes their inputs.
-      const int part = k == 0 ? 0 : k == 4 ? 1 : k == 5 ? 2 : -1;
+      const int part = k == 0 ? 0 : k == 4 ? 1 : k == 5 ? 3 : -1;
       if (part >= 0) {
         HIP_TRY(hipEventRecord(S->ev_j0, s0));
         HIP_TRY(hipEventRecord(S->ev_j1, s1));
         HIP_TRY(hipStreamWaitEvent(S->aux, S->ev_j0, 0));
         HIP_TRY(hipStreamWaitEvent(S->aux, S->ev_j1, 0));
         TRY(block_param_grads(S, l, part, A, xin, dyl, B, d1, d2, grads, accumulate, S->aux));
+        if (part == 1) TRY(block_param_grads(S, l, 2, A, xin, dyl, B, d1, d2, grads, accumulate, S->aux));
       }
     }
     HIP_TRY(hipEventRecord(S->ev_dw[par], S->aux));
