@@ -651,12 +651,15 @@ static long long tile_count(const GemmBatch& b, int bm, int bn) {
 // Tile choice (measured on MI355X with random bf16 data, isolated, as two
 // concurrent launches, and inside the two-stream stage step).  Large tiles on
 // 8 waves (two per SIMD) move the fewest operand bytes per FLOP through L2 and
-// LDS: the input-gradient GEMMs (B read in place from the [out, in] weights)
-// run as 256 x 256 tiles, every other GEMM with at least 128 such tiles as
+// LDS: the input- and weight-gradient GEMMs (B read with M/N contiguous) run
+// as 256 x 256 tiles, every other GEMM with at least 128 such tiles as
 // 256 x 192 tiles.  Narrow problems (the projection's input gradient, N = h/t)
 // keep 128 x 192 tiles on 4 waves so that the grid still covers most CUs.
 // Against 128 x 192 tiles everywhere the stage step measured +6.3% (819 ->
-// 870 TFLOP/s); 256 x 256 tiles everywhere +3.6%, 256 x 192 everywhere +5.3%.
+// 870 TFLOP/s); 256 x 256 tiles everywhere +3.6%, 256 x 192 everywhere +5.3%
+// (before the instruction order of the main loop above); with that order,
+// 256 x 256 for the weight gradients added 0.6%, while 256 x 192 for the
+// smaller (QKV / projection) weight-gradient group lost 0.6%.
 static int choose_tile(const GemmBatch& b, bool a_t, bool b_t) {
   if (g_tile_override != TILE_AUTO) return g_tile_override;
   if (b_t && tile_count(b, 256, 256) >= 128) return TILE_256x256_W8_S2;
