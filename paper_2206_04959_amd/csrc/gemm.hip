@@ -515,7 +515,9 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_mfma_kernel(GemmBatch batch
       for (int g = 0; g < 4; ++g)
         *reinterpret_cast<f32x4_t*>(stg + (lane & 31) * CLD + j * 32 + g * 8 + (lane >> 5) * 4) =
             f32x4_t{acc[j][i][4 * g], acc[j][i][4 * g + 1], acc[j][i][4 * g + 2], acc[j][i][4 * g + 3]};
-    __syncthreads();
+    // The staging tile is this wave's own: its LDS accesses complete in order,
+    // so a wait for its own writes (not a workgroup barrier) orders them.
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 #pragma unroll
     for (int u = 0; u < CPL; ++u) {
       const int q = lane + 64 * u;
@@ -532,7 +534,7 @@ __global__ void __launch_bounds__(WM * WN * 64) gemm_mfma_kernel(GemmBatch batch
         else epilogue8<bf16_t, EPI>(p, m, n, v);
       }
     }
-    __syncthreads();  // the slab is read before the next one overwrites it
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the slab is read before the next one overwrites it
   }
 }
 
