@@ -174,13 +174,17 @@ def test_attention_fwd_bwd(dtype, d, seq, batch, heads):
 
 @pytest.mark.parametrize("cfg", list(range(1, 11)))
 @pytest.mark.parametrize("a_t,b_t", [(0, 0), (0, 1), (1, 1), (1, 0)])
-def test_gemm_every_tile_shape(cfg, a_t, b_t):
+@pytest.mark.parametrize("K", [64, 192, 320])
+def test_gemm_every_tile_shape(cfg, a_t, b_t, K):
     """Each tile shape of the bf16 kernel on a ragged problem (M, N not
-    multiples of 128 or 256; K spans 5 stages), fp32 output so the check is
-    tight."""
+    multiples of 128 or 256), fp32 output so the check is tight.  K spans 1,
+    3 or 5 stages of 64: fewer stages than the LDS ring holds, as many as a
+    3-stage ring, and more, so that every path of the load schedule (loads
+    issued in the prologue only, split over the two sub-steps after a
+    barrier, none for the last stages) runs."""
     torch = need_gpu()
-    M, N, K = 320, 448, 320
-    print(f"[gemm tile {cfg}] a_t={a_t} b_t={b_t}", flush=True)
+    M, N = 320, 448
+    print(f"[gemm tile {cfg}] a_t={a_t} b_t={b_t} K={K}", flush=True)
     a_p, a = _rand((K, M) if a_t else (M, K), "bf16", 21)
     b_p, b = _rand((K, N) if b_t else (N, K), "bf16", 22)
     ref = (a.T if a_t else a) @ (b if b_t else b.T)
