@@ -10,7 +10,9 @@
 // banks of gfx950 LDS; operands contiguous along M or N stay that way in LDS
 // and are read with the transposing LDS read, so no operand is transposed in
 // registers.  Each wave reads the fragments of the next K sub-step while the
-// MFMAs of the current one run, with one workgroup barrier per K stage.  The
+// MFMAs of the current one run, with one workgroup barrier per K stage; the
+// fragment reads and the loads of later stages are issued one at a time
+// between the MFMAs rather than in bursts.  The
 // MFMA takes the B tile as its first operand so each lane owns one output row
 // and 4 consecutive columns per group, which the fused epilogues store as one
 // vector.  Workgroups are mapped to tiles so that each of the 8 XCDs works on
