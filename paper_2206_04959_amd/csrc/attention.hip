@@ -43,11 +43,14 @@ typedef short s16x4_t __attribute__((ext_vector_type(4)));
 typedef short s16x8_t __attribute__((ext_vector_type(8)));
 #define MERAK_LDS __attribute__((address_space(3)))
 
+// Eight accumulator values narrowed to an MFMA operand, four packed
+// conversion instructions.
 __device__ __forceinline__ bf16x8_t cvt8(const f32x16_t& a, int base) {
-  bf16x8_t r;
+  typedef float f32x8_t __attribute__((ext_vector_type(8)));
+  f32x8_t v;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) r[e] = (__bf16)a[base + e];
-  return r;
+  for (int e = 0; e < 8; ++e) v[e] = a[base + e];
+  return __builtin_convertvector(v, bf16x8_t);
 }
 
 // A [64 rows][D] bf16 tile in LDS with rows padded to LD elements: 16-byte
@@ -444,6 +447,10 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_bf16(int S, int H, int Bm, 
     // register set); each dK/dV accumulator still takes its four 16-query
     // groups in order 0..3, so the sums are those of the whole block.
     const bool diag = qs < kw0 + 32;  // some query of the block precedes some key of the wave
+    // Query qs + qi precedes this lane's key iff qi < key - qs.  With the lane's
+    // part of qi (4 hf) folded in, one compare against a constant per score
+    // decides; off the diagonal the limit is below every qi and masks nothing.
+    const int mlim = (diag ? key - qs : -1) - hf * 4;
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       f32x16_t p, dp;
@@ -459,9 +466,10 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_bf16(int S, int H, int Bm, 
       // p[r]: query qs + t*32 + (r/4)*8 + 4*hf + r%4, key `key`.
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int qi = t * 32 + (r >> 2) * 8 + hf * 4 + (r & 3);
+        const int qc = t * 32 + (r >> 2) * 8 + (r & 3);
+        const int qi = qc + hf * 4;
         float pv = __builtin_amdgcn_exp2f(fmaf(p[r], scale_log2, -lse_s[qi]));
-        if (diag && key > qs + qi) pv = 0.0f;
+        if (qc < mlim) pv = 0.0f;
         p[r] = pv;
         dp[r] = pv * (dp[r] - del_s[qi]);
       }
@@ -797,15 +805,10 @@ MERAK_ATTN_INST(96)
 MERAK_ATTN_INST(128)
 #undef MERAK_ATTN_INST
 
-// Allow a kernel's dynamic LDS beyond the default limit (once per instantiation;
-// the call is idempotent, so host threads racing on the first launch are harmless).
+// Allow a kernel's dynamic LDS beyond the default limit on the current device.
 template <typename K>
-static hipError_t allow_lds(K kern, size_t bytes, std::atomic<bool>& done) {
-  if (done.load(std::memory_order_acquire)) return hipSuccess;
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
-                                     (int)bytes);
-  if (e == hipSuccess) done.store(true, std::memory_order_release);
-  return e;
+static hipError_t allow_lds(K kern, size_t bytes, std::atomic<uint64_t>& done) {
+  return allow_dynamic_lds(reinterpret_cast<const void*>(kern), bytes, done);
 }
 
 template <int D>
@@ -814,7 +817,7 @@ static hipError_t fwd_d(int dtype, int B, int S, int H, int G, int mstride, cons
   const float scale = 1.0f / sqrtf((float)D);
   if (dtype == DT_BF16) {
     constexpr size_t lds = attn_lds_bytes<D>();
-    static std::atomic<bool> ok{false};
+    static std::atomic<uint64_t> ok{0};
     hipError_t e = allow_lds(attn_fwd_bf16<D>, lds, ok);
     if (e != hipSuccess) return e;
     dim3 grid(H, G * B, S / 64);
@@ -841,7 +844,7 @@ static hipError_t bwd_d(int dtype, int B, int S, int H, int G, int mstride, cons
     constexpr size_t lds_q = attn_lds_bytes<D>();
     constexpr size_t lds_k = attn_lds_bytes<D>() + kAttnStages * 256 * sizeof(float);
     static_assert(lds_k <= 160 * 1024, "LDS budget");
-    static std::atomic<bool> ok_k{false}, ok_q{false};
+    static std::atomic<uint64_t> ok_k{0}, ok_q{0};
     hipError_t e = allow_lds(attn_bwd_dkdv_bf16<D>, lds_k, ok_k);
     if (e == hipSuccess) e = allow_lds(attn_bwd_dq_bf16<D>, lds_q, ok_q);
     if (e != hipSuccess) return e;

@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 namespace merak {
 
 typedef uint16_t bf16_t;  // bf16 storage (bit pattern)
@@ -48,8 +50,11 @@ __device__ __forceinline__ void load4(const float* p, float v[4]) {
   f32x4_t r = *reinterpret_cast<const f32x4_t*>(p);
   v[0] = r[0]; v[1] = r[1]; v[2] = r[2]; v[3] = r[3];
 }
+// Two values narrowed by one packed conversion instruction (converting them
+// one at a time costs two conversions plus a shift and an OR).
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return (uint32_t)f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
 }
 __device__ __forceinline__ void store4(bf16_t* p, const float v[4]) {
   *reinterpret_cast<u32x2_t*>(p) = u32x2_t{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
@@ -111,6 +116,22 @@ __device__ __forceinline__ float gelu_f(float u) { return u * gelu_sigmoid(u); }
 __device__ __forceinline__ float gelu_grad_f(float u) {
   const float s = gelu_sigmoid(u);
   return s + 2.0f * u * s * (1.0f - s) * kGeluC * (1.0f + 3.0f * kGeluA * u * u);
+}
+
+// Host side: allow a kernel `bytes` of dynamic LDS beyond the default limit on
+// the current device.  The attribute is held per device, so it is set once for
+// each device the kernel runs on (bit d of `done`; devices past 63 set it on
+// every launch).  The call is idempotent, so host threads racing on a first
+// launch are harmless.
+inline hipError_t allow_dynamic_lds(const void* kern, size_t bytes, std::atomic<uint64_t>& done) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  const uint64_t bit = dev >= 0 && dev < 64 ? (uint64_t)1 << dev : 0;
+  if (bit && (done.load(std::memory_order_acquire) & bit)) return hipSuccess;
+  e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+  if (e == hipSuccess && bit) done.fetch_or(bit, std::memory_order_acq_rel);
+  return e;
 }
 
 }  // namespace merak

@@ -607,10 +607,8 @@ static hipError_t run_mfma(GemmBatch& batch, hipStream_t stream) {
   constexpr size_t lds = (size_t)NS * (BM + BN) * 128;
   static_assert(lds <= 160 * 1024, "LDS budget");
   auto kern = gemm_mfma_kernel<BM, BN, WM, WN, NS, AT, BT, EPI>;
-  // Once per instantiation; the initialisation of a function-local static is
-  // thread-safe, so concurrent first launches from several host threads agree.
-  static const hipError_t attr_err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  static std::atomic<uint64_t> lds_set{0};  // devices this instantiation's LDS limit is set on
+  const hipError_t attr_err = allow_dynamic_lds(reinterpret_cast<const void*>(kern), lds, lds_set);
   if (attr_err != hipSuccess) return attr_err;
   hipLaunchKernelGGL(kern, dim3(tiles), dim3(WM * WN * 64), lds, stream, batch);
   return hipGetLastError();
