@@ -655,17 +655,23 @@ static long long tile_count(const GemmBatch& b, int bm, int bn) {
 // 8 waves (two per SIMD) move the fewest operand bytes per FLOP through L2 and
 // LDS: the input- and weight-gradient GEMMs (B read with M/N contiguous) run
 // as 256 x 256 tiles, every other GEMM with at least 128 such tiles as
-// 256 x 192 tiles.  Narrow problems (the projection's input gradient, N = h/t)
-// keep 128 x 192 tiles on 4 waves so that the grid still covers most CUs.
-// Against 128 x 192 tiles everywhere the stage step measured +6.3% (819 ->
-// 870 TFLOP/s); 256 x 256 tiles everywhere +3.6%, 256 x 192 everywhere +5.3%
-// (before the instruction order of the main loop above); with that order,
-// 256 x 256 for the weight gradients added 0.6%, while 256 x 192 for the
-// smaller (QKV / projection) weight-gradient group lost 0.6%.
+// 256 x 192 tiles.  Narrower problems (most GEMMs of stages with 2048-row
+// sub-micro-batches) run as 256 x 128 tiles on 8 waves with a 3-stage ring
+// while that still gives at least 100 tiles; the narrowest (the projection's
+// input gradient at N = h/t = 768) keep 128 x 192 tiles on 4 waves, whose
+// larger grid is faster alone and the same in the stage.  Against 128 x 192
+// tiles everywhere the stage step measured +6.3% (819 -> 870 TFLOP/s);
+// 256 x 256 tiles everywhere +3.6%, 256 x 192 everywhere +5.3% (before the
+// instruction order of the main loop above); with that order, 256 x 256 for
+// the weight gradients added 0.6%, while 256 x 192 for the smaller (QKV /
+// projection) weight-gradient group lost 0.6%.  The 256 x 128 rule: +2.9% on
+// the 1.5B-shaped stage, +1.8% on the 2.5B-shaped shard (their hidden sizes
+// 1600 and 1920 make most of their GEMMs narrow), no change elsewhere.
 static int choose_tile(const GemmBatch& b, bool a_t, bool b_t) {
   if (g_tile_override != TILE_AUTO) return g_tile_override;
   if (b_t && tile_count(b, 256, 256) >= 128) return TILE_256x256_W8_S2;
   if (tile_count(b, 256, 192) >= 128) return TILE_256x192_W8_S2;
+  if (tile_count(b, 256, 128) >= 100) return TILE_256x128_W8_S3;
   return TILE_128x192_W4_S2;
 }
 

@@ -50,7 +50,7 @@ def test_gemm_kernels_do_not_spill():
     spills = {k: v["ScratchSize"] for k, v in mfma.items() if v.get("ScratchSize", 0) != 0}
     assert not spills, spills
     # the eight-wave tiles the stage uses run two waves per SIMD
-    for shape in ("ILi256ELi256ELi2ELi4ELi2E", "ILi256ELi192ELi4ELi2ELi2E"):
+    for shape in ("ILi256ELi256ELi2ELi4ELi2E", "ILi256ELi192ELi4ELi2ELi2E", "ILi256ELi128ELi4ELi2ELi3E"):
         occ = {k: v["Occupancy"] for k, v in mfma.items() if shape in k}
         assert occ and min(occ.values()) >= 2, occ
 
