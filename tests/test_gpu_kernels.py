@@ -56,9 +56,23 @@ def test_gemm_layouts(dtype, a_t, b_t, mnk):
     assert rel_err(c32.cpu().numpy(), 2 * ref) < 2e-5
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
-def test_gemm_epilogues(dtype):
+# bf16: the automatic tile choice and each tile the stage's choice can make
+# (256x256, 256x128 and 128x192 tiles, 256x192); fp32 has one kernel.
+EPI_CASES = [("bf16", 0), ("bf16", 7), ("bf16", 8), ("bf16", 9), ("bf16", 10), ("fp32", 0)]
+
+
+@pytest.mark.parametrize("dtype,tile", EPI_CASES)
+def test_gemm_epilogues(dtype, tile):
     torch = need_gpu()
+    print(f"[gemm epilogues] {dtype} tile {tile}", flush=True)
+    prev = B.gemm_tile_override(tile)
+    try:
+        _gemm_epilogues(torch, dtype)
+    finally:
+        B.gemm_tile_override(prev)
+
+
+def _gemm_epilogues(torch, dtype):
     M, N, K = 320, 448, 192
     a_p, a = _rand((M, K), dtype, 3)
     w_p, w = _rand((N, K), dtype, 4, std=0.1)
