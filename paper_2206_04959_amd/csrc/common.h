@@ -1,5 +1,6 @@
-// Device-side helpers shared by the gfx950 kernels: storage types, bf16
-// conversion, vector loads/stores, wave64 reductions and MFMA operand types.
+// Helpers shared by the gfx950 kernels: storage types, bf16 conversion,
+// vector loads/stores, wave64 reductions and MFMA operand types (device side),
+// and the per-device dynamic-LDS attribute (host side).
 #pragma once
 
 #include <hip/hip_runtime.h>
