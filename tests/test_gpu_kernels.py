@@ -152,6 +152,7 @@ def test_column_sum(dtype):
 
 ATTN_CASES = [(dt, d, s, 2, 3) for dt in ("bf16", "fp32") for d in (64, 96, 128) for s in (128, 320)]
 ATTN_CASES += [("bf16", 128, 2048, 1, 2), ("bf16", 96, 1024, 2, 2)]  # full-length rows of the workloads
+ATTN_CASES += [("bf16", d, 64, 2, 3) for d in (64, 96, 128)]  # one block: the pair's second half is empty
 
 
 @pytest.mark.parametrize("dtype,d,seq,batch,heads", ATTN_CASES)
