@@ -29,6 +29,13 @@ SMALL = {
     # the per-stream grouped launches have unequal member counts
     "d64-n3-bf16": synth.StageShape("d64n3", n_blocks=2, hidden=256, n_heads=4, ffn=1024, seq_len=128,
                                     micro_batch=6, tp_degree=1, n_sub=3, recompute_mask=0b10, seed=35),
+    # the smallest stage the boundary accepts: one block, one head of 64, one
+    # 64-token sequence (every GEMM a single partial tile, one attention block,
+    # one reduction segment)
+    "min-bf16": synth.StageShape("min", n_blocks=1, hidden=64, n_heads=1, ffn=64, seq_len=64, micro_batch=1,
+                                 tp_degree=1, n_sub=1, recompute_mask=0b1, seed=36),
+    "min-fp32": synth.StageShape("minf", n_blocks=1, hidden=64, n_heads=1, ffn=64, seq_len=64, micro_batch=1,
+                                 tp_degree=1, n_sub=1, recompute_mask=0b0, dtype="fp32", seed=37),
 }
 
 
