@@ -360,6 +360,8 @@ int merak_graph_shard(int n_nodes, const int32_t* kind, const int64_t* params, c
  * They exist so each kernel can be checked and timed on its own; the stage
  * calls above use the same kernels.  dtype is merak_dtype; pointers follow the
  * conventions above (16-byte aligned).  No entry point allocates memory.
+ * Every size argument must be positive: an empty input (rows, M, N, K, seq,
+ * batch or heads of 0) returns MERAK_ERR_SHAPE with nothing enqueued.
  * ---------------------------------------------------------------------- */
 
 /* GEMM epilogues. */
@@ -377,7 +379,7 @@ typedef enum {
  *   a_trans = 0: A[m,k] at a[m*lda + k];  1: A[m,k] at a[k*lda + m].
  *   b_trans = 0: B[k,n] at b[n*ldb + k] (a weight [N,K]: "X W^T");
  *             1: B[k,n] at b[k*ldb + n].
- * M, N, K must be multiples of 64 and lda, ldb multiples of 8 (else
+ * M, N, K must be positive multiples of 64 and lda, ldb multiples of 8 (else
  * MERAK_ERR_SHAPE).  C, resid and aux are [M, N] row-major (ld = N); bias is
  * [N].  Elements are of `dtype` except C for MERAK_EPI_F32 (always fp32). */
 int merak_gemm(int dtype, int a_trans, int b_trans, int epilogue, int M, int N, int K,

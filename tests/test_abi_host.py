@@ -138,3 +138,18 @@ def test_kernel_entry_points_validate_before_launch():
     assert lib.merak_column_sum(0, 4, 64, p, p, 2, p, None) == -1
     assert B.reduce_scratch_elems(128, 10) == 2 * 10
     assert B.reduce_scratch_elems(0, 10) == 0
+
+
+def test_kernel_entry_points_reject_empty_inputs():
+    """A size of 0 is refused before anything is launched (no GPU needed)."""
+    lib = B.lib()
+    p = 0x100000
+    for M, N, K in ((0, 64, 64), (64, 0, 64), (64, 64, 0)):
+        assert lib.merak_gemm(0, 0, 0, 0, M, N, K, p, 64, p, 64, p, None, None, None, 0, None) == -2
+    assert lib.merak_layernorm_fwd(0, 0, 64, 1e-5, p, p, p, p, p, p, None) == -2
+    assert lib.merak_layernorm_bwd(0, 0, 64, p, p, p, p, p, p, p, p, p, 0, p, None) == -2
+    assert lib.merak_layernorm_bwd_noalloc(0, 0, 64, p, p, p, p, p, p, p, p, p, 0, None) == -2
+    assert lib.merak_column_sum(0, 0, 64, p, p, 0, p, None) == -2
+    for batch, seq, heads in ((0, 64, 1), (1, 0, 1), (1, 64, 0)):
+        assert lib.merak_attention_fwd(0, batch, seq, heads, 64, p, p, p, None) == -2
+        assert lib.merak_attention_bwd(0, batch, seq, heads, 64, p, p, p, p, p, p, None) == -2
