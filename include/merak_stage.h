@@ -85,7 +85,10 @@ typedef enum { MERAK_BF16 = 0, MERAK_FP32 = 1 } merak_dtype;
  * Constraints (else MERAK_ERR_SHAPE): 1 <= n_blocks <= 64; n_heads % tp_degree
  * == 0; hidden % n_heads == 0; ffn % tp_degree == 0; micro_batch %
  * n_sub_microbatches == 0; hidden, hidden/tp_degree, ffn/tp_degree and
- * seq_len multiples of 64; recompute_mask has no bit >= n_blocks; ln_eps > 0.
+ * seq_len multiples of 64; recompute_mask has no bit >= n_blocks; ln_eps > 0;
+ * micro_batch*seq_len times ffn/tp_degree and times 3*hidden below 2^31; in
+ * MERAK_BF16, (micro_batch*seq_len + 256) * max(hidden, 3*hidden/tp_degree,
+ * ffn/tp_degree) * 2 bytes below 2^31 (the GEMM's 32-bit operand offsets).
  * head_dim = hidden/n_heads must be 64, 96 or 128 (else MERAK_ERR_UNSUPPORTED). */
 typedef struct {
   int32_t n_blocks;           /* L: blocks in the stage                               */
@@ -379,8 +382,9 @@ typedef enum {
  *   a_trans = 0: A[m,k] at a[m*lda + k];  1: A[m,k] at a[k*lda + m].
  *   b_trans = 0: B[k,n] at b[n*ldb + k] (a weight [N,K]: "X W^T");
  *             1: B[k,n] at b[k*ldb + n].
- * M, N, K must be positive multiples of 64 and lda, ldb multiples of 8 (else
- * MERAK_ERR_SHAPE).  C, resid and aux are [M, N] row-major (ld = N); bias is
+ * M, N, K must be positive multiples of 64 and lda, ldb multiples of 8, and in
+ * MERAK_BF16 each operand, counted with 256 rows of edge-tile padding past M
+ * (or N), must span fewer than 2^31 bytes (else MERAK_ERR_SHAPE).  C, resid and aux are [M, N] row-major (ld = N); bias is
  * [N].  Elements are of `dtype` except C for MERAK_EPI_F32 (always fp32). */
 int merak_gemm(int dtype, int a_trans, int b_trans, int epilogue, int M, int N, int K,
                const void* a, int lda, const void* b, int ldb, void* c, const void* bias,

@@ -712,14 +712,8 @@ static hipError_t dispatch_epi(int dtype, int epi, GemmBatch& batch, hipStream_t
 hipError_t launch_gemm(int dtype, bool a_t, bool b_t, int epi, const GemmProblem* probs, int n_probs,
                        hipStream_t stream) {
   if (n_probs < 1 || n_probs > kMaxGroup) return hipErrorInvalidValue;
-  // The bf16 kernel addresses each operand with 32-bit byte offsets, including
-  // the rows of a partial edge tile.
-  for (int i = 0; i < n_probs; ++i) {
-    const GemmProblem& q = probs[i];
-    const long long ea = (long long)(a_t ? q.K : q.M + 256) * q.lda + (a_t ? q.M + 256 : q.K);
-    const long long eb = (long long)(b_t ? q.K : q.N + 256) * q.ldb + (b_t ? q.N + 256 : q.K);
-    if (dtype == DT_BF16 && (2 * ea >= (1LL << 31) || 2 * eb >= (1LL << 31))) return hipErrorInvalidValue;
-  }
+  for (int i = 0; i < n_probs; ++i)
+    if (dtype == DT_BF16 && !gemm_bf16_offsets_fit(probs[i], a_t, b_t)) return hipErrorInvalidValue;
   GemmBatch batch;
   for (int i = 0; i < n_probs; ++i) batch.p[i] = probs[i];
   batch.n_probs = n_probs;

@@ -38,6 +38,14 @@ constexpr int kMaxGroup = 4;
 // as one grid.
 hipError_t launch_gemm(int dtype, bool a_t, bool b_t, int epi, const GemmProblem* probs, int n_probs,
                        hipStream_t stream);
+// Whether the bf16 kernel can address both operands of `q`: it uses 32-bit
+// byte offsets, counting the rows of a partial edge tile (up to 256 past M or
+// N).  launch_gemm refuses a problem that does not fit.
+inline bool gemm_bf16_offsets_fit(const GemmProblem& q, bool a_t, bool b_t) {
+  const long long ea = (long long)(a_t ? q.K : q.M + 256) * q.lda + (a_t ? q.M + 256 : q.K);
+  const long long eb = (long long)(b_t ? q.K : q.N + 256) * q.ldb + (b_t ? q.N + 256 : q.K);
+  return 2 * ea < (1LL << 31) && 2 * eb < (1LL << 31);
+}
 
 // LayerNorm over rows of width h (h % 8 == 0).  Like attention, one launch may
 // cover `members` groups of `rows` rows, member m starting m * member_stride

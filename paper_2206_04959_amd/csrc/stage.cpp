@@ -68,6 +68,14 @@ int check_config(const merak_stage_config* c) {
   const int64_t T = (int64_t)c->micro_batch * c->seq_len;
   if (T * (int64_t)c->ffn / c->tp_degree >= ((int64_t)1 << 31) || T * (int64_t)c->hidden * 3 >= ((int64_t)1 << 31))
     return MERAK_ERR_SHAPE;
+  // The bf16 GEMM addresses each [T, width] activation operand with 32-bit
+  // byte offsets, 256 rows of edge-tile padding included (the weight-gradient
+  // GEMMs read the whole micro-batch as one operand).
+  if (c->dtype == MERAK_BF16) {
+    const int64_t hl = c->hidden / c->tp_degree, fl = c->ffn / c->tp_degree;
+    const int64_t w = std::max<int64_t>(std::max<int64_t>(c->hidden, fl), 3 * hl);
+    if (2 * ((T + 256) * w + w) >= ((int64_t)1 << 31)) return MERAK_ERR_SHAPE;
+  }
   const int d = c->hidden / c->n_heads;
   if (d != 64 && d != 96 && d != 128) return MERAK_ERR_UNSUPPORTED;
   return MERAK_OK;
@@ -1113,6 +1121,7 @@ int merak_gemm(int dtype, int a_trans, int b_trans, int epilogue, int M, int N, 
   if (aux && !aligned(aux, 16)) return MERAK_ERR_ALIGN;
   if (accumulate != 0 && accumulate != 1) return MERAK_ERR_INVALID_ARG;
   GemmProblem p = gp(M, N, K, a, lda, b, ldb, c, N, bias, resid, aux, accumulate);
+  if (dtype == MERAK_BF16 && !gemm_bf16_offsets_fit(p, a_trans, b_trans)) return MERAK_ERR_SHAPE;
   HIP_TRY(launch_gemm(dtype, a_trans, b_trans, epilogue, &p, 1, (hipStream_t)stream));
   return MERAK_OK;
 }

@@ -50,6 +50,9 @@ def test_presets_validate(name):
     (dict(recompute_mask=0b10), -2),            # bit >= n_blocks
     (dict(ln_eps=0.0), -2),
     (dict(hidden=192, n_heads=2, ffn=768, tp_degree=2), -2),  # h/t = 96 not a multiple of 64
+    # bf16: a [b*s, ffn] activation of 2^20 rows (+256 rows of tile padding) passes 2^31 bytes;
+    # the fp32 check mode has no such limit
+    (dict(micro_batch=8192, dtype="bf16"), -2), (dict(micro_batch=8192, dtype="fp32"), 0),
 ])
 def test_bad_configs_rejected(change, status):
     cfg = B.make_config(synth.TINY.replace(**change))
@@ -138,6 +141,15 @@ def test_kernel_entry_points_validate_before_launch():
     assert lib.merak_column_sum(0, 4, 64, p, p, 2, p, None) == -1
     assert B.reduce_scratch_elems(128, 10) == 2 * 10
     assert B.reduce_scratch_elems(0, 10) == 0
+
+
+def test_gemm_rejects_operands_beyond_its_offsets():
+    """bf16 operands past 2^31 bytes (with 256 rows of padding) are a shape error, found
+    before any launch; the fp32 kernel indexes with 64 bits."""
+    lib = B.lib()
+    p = 0x100000
+    assert lib.merak_gemm(0, 0, 0, 0, 1 << 19, 64, 2048, p, 2048, p, 2048, p, None, None, None, 0, None) == -2
+    assert lib.merak_gemm(0, 1, 0, 0, 64, 64, 1 << 20, p, 1024, p, 1 << 20, p, None, None, None, 0, None) == -2
 
 
 def test_kernel_entry_points_reject_empty_inputs():
