@@ -438,6 +438,13 @@ size_t merak_noalloc_scratch_elems(void);
 int merak_column_sum(int dtype, int rows, int cols, const void* x, float* out, int accumulate,
                      float* scratch, void* stream);
 
+/* Failure detection: the number of NaN and +-Inf elements among the n elements
+ * of x (dtype; 16-byte aligned unless n = 0) is written to *count, a device
+ * uint64 (16-byte aligned) that the call overwrites; read it after the stream
+ * has reached the call.  n = 0 writes 0.  An integer count, so it does not
+ * depend on timing.  Enqueues two kernels and allocates nothing. */
+int merak_count_nonfinite(int dtype, const void* x, int64_t n, uint64_t* count, void* stream);
+
 /* Causal attention forward on a packed qkv buffer [batch, seq, 3, heads, d]
  * (row stride 3*heads*d, the QKV GEMM's output layout): o [batch, seq, heads, d]
  * and lse fp32 [batch, heads, seq] = natural log of sum_j exp(q_i k_j / sqrt(d))

@@ -72,6 +72,7 @@ _SIGS = {
     "merak_layernorm_bwd_noalloc": ([_I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _P], _I),
     "merak_noalloc_scratch_elems": ([], _SZ),
     "merak_column_sum": ([_I, _I, _I, _P, _P, _I, _P, _P], _I),
+    "merak_count_nonfinite": ([_I, _P, ctypes.c_int64, _P, _P], _I),
     "merak_attention_fwd": ([_I, _I, _I, _I, _I, _P, _P, _P, _P], _I),
     "merak_attention_bwd": ([_I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P], _I),
 }
@@ -353,6 +354,15 @@ def column_sum(x, out, scratch, accumulate=False, stream=None) -> None:
     rows, cols = x.shape
     _check(lib().merak_column_sum(_dt(x), rows, cols, _ptr(x), _ptr(out), int(accumulate), _ptr(scratch),
                                   _stream(stream)), "merak_column_sum")
+
+
+def count_nonfinite(x, count, stream=None) -> None:
+    """Enqueue the count of NaN/Inf elements of tensor x into count (a device int64 tensor of one element)."""
+    import torch
+    if x.dtype not in (torch.bfloat16, torch.float32) or count.dtype != torch.int64 or count.numel() != 1:
+        raise ValueError("count_nonfinite: x bf16 or fp32, count one int64 element")
+    _check(lib().merak_count_nonfinite(_dt(x), _ptr(x), x.numel(), _ptr(count), _stream(stream)),
+           "merak_count_nonfinite")
 
 
 def attention_fwd(qkv, o, lse, batch, seq, heads, head_dim, stream=None) -> None:

@@ -99,6 +99,12 @@ struct ReduceJob {
 };
 hipError_t launch_reduce_partials_batch(const ReduceJob* jobs, int n, hipStream_t stream);
 
+// Count of the NaN and +-Inf elements among x[0 .. n) into *count (device,
+// 64-bit; the first kernel sets it to zero, so no memset node is needed under
+// graph capture).  x is 16-byte aligned.
+hipError_t launch_count_nonfinite(int dtype, const void* x, long long n, unsigned long long* count,
+                                  hipStream_t stream);
+
 // Library-owned scratch of the allocation-free LayerNorm backward
 // (merak_layernorm_bwd_noalloc): kNoAllocScratchFloats fp32 elements per GPU.
 // noalloc_scratch returns its device address on the current device, taking it

@@ -10,6 +10,7 @@
 // kReduceRows rows and a 512-column slice, its 4 waves take every 4th row of
 // the segment, and their register sums are added in wave order into one
 // partial row; reduce_partials then adds the partials in segment order.
+#include <algorithm>
 #include <atomic>
 #include <mutex>
 
@@ -398,6 +399,67 @@ hipError_t launch_reduce_partials(int groups, int cols, const float* part, float
 // hipGetSymbolAddress and kept per device.
 // ---------------------------------------------------------------------------
 static __device__ __align__(256) float scratch[kNoAllocScratchFloats];
+
+// ---------------------------------------------------------------------------
+// Non-finite scan (failure detection): an element is NaN or +-Inf iff its
+// exponent field is all ones (bf16: bits 7..14, fp32: bits 23..30).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ unsigned nonfinite_bf16_pair(uint32_t w) {
+  return ((w & 0x7f80u) == 0x7f80u) + ((w & 0x7f800000u) == 0x7f800000u);
+}
+__device__ __forceinline__ unsigned nonfinite_f32(uint32_t w) { return (w & 0x7f800000u) == 0x7f800000u; }
+
+__global__ void __launch_bounds__(64) zero_count_kernel(unsigned long long* count) {
+  if (threadIdx.x == 0) *count = 0ull;
+}
+
+// Grid-stride over 16-byte chunks; the elements past the last whole chunk are
+// taken by workgroup 0.  Per-thread counts are summed in LDS, then one atomic
+// add per workgroup: an integer sum, so the result does not depend on order.
+template <bool BF16>
+__global__ void __launch_bounds__(256) count_nonfinite_kernel(const uint32_t* __restrict__ x, long long n,
+                                                              unsigned long long* __restrict__ count) {
+  __shared__ unsigned long long blk;
+  constexpr int PER = BF16 ? 8 : 4;  // elements per 16-byte chunk
+  const long long chunks = n / PER;
+  unsigned long long c = 0;
+  const long long stride = (long long)gridDim.x * blockDim.x;
+  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < chunks; i += stride) {
+    const u32x4_t w = reinterpret_cast<const u32x4_t*>(x)[i];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) c += BF16 ? nonfinite_bf16_pair(w[e]) : nonfinite_f32(w[e]);
+  }
+  if (blockIdx.x == 0) {
+    for (long long i = chunks * PER + threadIdx.x; i < n; i += blockDim.x) {
+      if constexpr (BF16) {
+        const uint16_t v = reinterpret_cast<const uint16_t*>(x)[i];
+        c += (v & 0x7f80u) == 0x7f80u;
+      } else {
+        c += nonfinite_f32(x[i]);
+      }
+    }
+  }
+  if (threadIdx.x == 0) blk = 0ull;
+  __syncthreads();
+  if (c) atomicAdd(&blk, c);
+  __syncthreads();
+  if (threadIdx.x == 0 && blk) atomicAdd(count, blk);
+}
+
+hipError_t launch_count_nonfinite(int dtype, const void* x, long long n, unsigned long long* count,
+                                  hipStream_t stream) {
+  hipLaunchKernelGGL(zero_count_kernel, dim3(1), dim3(64), 0, stream, count);
+  if (n <= 0) return hipGetLastError();
+  const long long chunks = n / (dtype == DT_BF16 ? 8 : 4);
+  const long long blocks = std::min<long long>(std::max<long long>((chunks + 255) / 256, 1), 2048);
+  if (dtype == DT_BF16)
+    hipLaunchKernelGGL((count_nonfinite_kernel<true>), dim3((unsigned)blocks), dim3(256), 0, stream,
+                       (const uint32_t*)x, n, count);
+  else
+    hipLaunchKernelGGL((count_nonfinite_kernel<false>), dim3((unsigned)blocks), dim3(256), 0, stream,
+                       (const uint32_t*)x, n, count);
+  return hipGetLastError();
+}
 
 namespace {
 constexpr int kMaxDevices = 64;

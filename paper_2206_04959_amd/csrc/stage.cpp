@@ -1196,6 +1196,15 @@ int merak_column_sum(int dtype, int rows, int cols, const void* x, float* out, i
   return MERAK_OK;
 }
 
+int merak_count_nonfinite(int dtype, const void* x, int64_t n, uint64_t* count, void* stream) {
+  if (dtype != MERAK_BF16 && dtype != MERAK_FP32) return MERAK_ERR_INVALID_ARG;
+  if (n < 0) return MERAK_ERR_SHAPE;
+  TRY(check_ptr(count));
+  if (n > 0) TRY(check_ptr(x));
+  HIP_TRY(launch_count_nonfinite(dtype, x, (long long)n, (unsigned long long*)count, (hipStream_t)stream));
+  return MERAK_OK;
+}
+
 int merak_attention_fwd(int dtype, int batch, int seq, int heads, int head_dim, const void* qkv, void* o, float* lse,
                         void* stream) {
   if (dtype != MERAK_BF16 && dtype != MERAK_FP32) return MERAK_ERR_INVALID_ARG;

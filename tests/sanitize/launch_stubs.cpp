@@ -18,6 +18,9 @@ hipError_t launch_reduce_partials(int, int, const float*, float*, int, hipStream
 hipError_t launch_column_partials_batch(int, const ColPartialJob*, int, hipStream_t) { return unreachable(); }
 hipError_t launch_reduce_partials_batch(const ReduceJob*, int, hipStream_t) { return unreachable(); }
 hipError_t noalloc_scratch(float**) { return unreachable(); }
+hipError_t launch_count_nonfinite(int, const void*, long long, unsigned long long*, hipStream_t) {
+  return unreachable();
+}
 hipError_t launch_attention_fwd(int, int, int, int, int, const void*, void*, float*, hipStream_t, int, int) {
   return unreachable();
 }

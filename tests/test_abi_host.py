@@ -152,6 +152,16 @@ def test_gemm_rejects_operands_beyond_its_offsets():
     assert lib.merak_gemm(0, 1, 0, 0, 64, 64, 1 << 20, p, 1024, p, 1 << 20, p, None, None, None, 0, None) == -2
 
 
+def test_count_nonfinite_validates_before_launch():
+    lib = B.lib()
+    p = 0x100000
+    assert lib.merak_count_nonfinite(2, p, 16, p, None) == -1      # dtype
+    assert lib.merak_count_nonfinite(0, p, -1, p, None) == -2      # negative size
+    assert lib.merak_count_nonfinite(0, p, 16, None, None) == -1   # no count
+    assert lib.merak_count_nonfinite(0, None, 16, p, None) == -1   # no input
+    assert lib.merak_count_nonfinite(0, p + 2, 16, p, None) == -4  # misaligned input
+
+
 def test_kernel_entry_points_reject_empty_inputs():
     """A size of 0 is refused before anything is launched (no GPU needed)."""
     lib = B.lib()

@@ -211,3 +211,33 @@ def test_gemm_every_tile_shape(cfg, a_t, b_t, K):
     finally:
         B.gemm_tile_override(prev)
     assert rel_err(c32.cpu().numpy(), ref) < 2e-5
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+@pytest.mark.parametrize("n", [0, 5, 4099, (1 << 20) + 7])
+def test_count_nonfinite(dtype, n):
+    """NaN and +-Inf planted at seeded positions (the ragged tail included),
+    beside the largest finite values and subnormals, are counted exactly."""
+    torch = need_gpu()
+    print(f"[nonfinite] {dtype} n={n}", flush=True)
+    rng = np.random.default_rng(90 + n)
+    v = rng.standard_normal(n).astype(np.float32)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    big = float(torch.finfo(tdt).max)
+    tiny = float(torch.finfo(tdt).tiny) / 4  # subnormal
+    if n:
+        idx = rng.choice(n, size=min(n, 37), replace=False)
+        kinds = [np.nan, np.inf, -np.inf, big, -big, tiny]
+        for j, i in enumerate(idx):
+            v[i] = kinds[j % len(kinds)]
+        v[n - 1] = np.nan  # the last element sits in the tail for most n
+    x = torch.from_numpy(v).to(tdt).to("cuda")
+    expect = int((~torch.isfinite(x.cpu().float())).sum().item())
+    count = torch.full((1,), -1, dtype=torch.int64, device="cuda")
+    B.count_nonfinite(x, count)
+    torch.cuda.synchronize()
+    assert int(count.item()) == expect
+    # a second call overwrites the count rather than adding to it
+    B.count_nonfinite(x, count)
+    torch.cuda.synchronize()
+    assert int(count.item()) == expect

@@ -194,3 +194,30 @@ def test_failed_launch_leaves_handle_refusing_dependent_calls():
     got = r.run().raw()
     for k in ref:
         assert np.array_equal(ref[k], got[k]), k
+
+
+@pytest.mark.parametrize("name", ["tiny-bf16", "tiny-fp32"])
+def test_nonfinite_scan_of_stage_outputs(name):
+    """Failure detection: a clean step leaves no NaN/Inf in y, dx or the
+    gradients; one NaN planted in the stage input (from the host) shows in the
+    scan of y, dx and the gradients."""
+    shape = SMALL[name]
+    print(f"[nonfinite scan] {name}", flush=True)
+    run = StageRun(shape)
+    torch = run.torch
+    count = torch.zeros(1, dtype=torch.int64, device="cuda")
+
+    def scan(t):
+        B.count_nonfinite(t, count)
+        torch.cuda.synchronize()
+        return int(count.item())
+
+    run.run()
+    assert scan(run.y) == 0 and scan(run.dx) == 0 and scan(run.grads) == 0
+    x = run.x.view(-1)
+    x[x.numel() // 3] = float("nan")  # one token's hidden state
+    torch.cuda.synchronize()
+    run.run()
+    ny, ndx, ng = scan(run.y), scan(run.dx), scan(run.grads)
+    print(f"  non-finite after one NaN in x: y {ny}, dx {ndx}, grads {ng}", flush=True)
+    assert ny >= shape.hidden and ndx > 0 and ng > 0
