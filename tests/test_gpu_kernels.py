@@ -105,11 +105,14 @@ def _gemm_epilogues(torch, dtype):
     assert rel_err(B.to_host_f64(c), acc * oracle.gelu_grad(u)) < tol
 
 
+# widths: the smallest (one 8-wide chunk, one active lane), ragged chunk counts,
+# the workloads' widths and the largest the kernels take (8192)
 @pytest.mark.parametrize("dtype", ["bf16", "fp32"])
-@pytest.mark.parametrize("h", [256, 1600, 3072, 6144])
+@pytest.mark.parametrize("h", [8, 256, 520, 1600, 3072, 6144, 8192])
 def test_layernorm_fwd_bwd(dtype, h):
     torch = need_gpu()
-    rows = 200
+    print(f"[layernorm] {dtype} h={h}", flush=True)
+    rows = 203  # a partial workgroup of rows and a partial 64-row reduction segment
     x_p, x = _rand((rows, h), dtype, 8, std=2.0, mean=0.5)
     g_p, g = _rand((h,), dtype, 9, std=0.1, mean=1.0)
     b_p, b = _rand((h,), dtype, 10, std=0.1)
