@@ -140,10 +140,13 @@ def test_layernorm_fwd_bwd(dtype, h):
     assert rel_err(db.cpu().numpy(), dbr) < 1e-5
 
 
+# one row of one 8-column chunk, a ragged column count over a partial
+# reduction segment, and a width past one workgroup's 512 columns
 @pytest.mark.parametrize("dtype", ["bf16", "fp32"])
-def test_column_sum(dtype):
+@pytest.mark.parametrize("rows,cols", [(1, 8), (1000, 776), (8192, 3072)])
+def test_column_sum(dtype, rows, cols):
     torch = need_gpu()
-    rows, cols = 1000, 776
+    print(f"[column sum] {dtype} {rows}x{cols}", flush=True)
     x_p, x = _rand((rows, cols), dtype, 13)
     out = torch.empty(cols, dtype=torch.float32, device="cuda")
     scratch = torch.empty(B.reduce_scratch_elems(rows, cols), dtype=torch.float32, device="cuda")
