@@ -56,6 +56,27 @@ def test_gemm_layouts(dtype, a_t, b_t, mnk):
     assert rel_err(c32.cpu().numpy(), 2 * ref) < 2e-5
 
 
+@pytest.mark.parametrize("cfg", list(range(1, 11)))
+@pytest.mark.parametrize("a_t,b_t", [(0, 0), (0, 1), (1, 1), (1, 0)])
+def test_gemm_smallest_problem_on_every_tile(cfg, a_t, b_t):
+    """M = N = K = 64, the smallest problem the boundary accepts: one partial
+    tile of every shape (up to 256 x 256), one K stage."""
+    torch = need_gpu()
+    M = N = K = 64
+    print(f"[gemm 64^3] tile {cfg} a_t={a_t} b_t={b_t}", flush=True)
+    a_p, a = _rand((K, M) if a_t else (M, K), "bf16", 23)
+    b_p, b = _rand((K, N) if b_t else (N, K), "bf16", 24)
+    ref = (a.T if a_t else a) @ (b if b_t else b.T)
+    c32 = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    prev = B.gemm_tile_override(cfg)
+    try:
+        B.gemm(_dev(a_p), _dev(b_p), c32, M, N, K, a_trans=a_t, b_trans=b_t, epilogue=B.EPI_F32, dtype=B.BF16)
+        torch.cuda.synchronize()
+    finally:
+        B.gemm_tile_override(prev)
+    assert rel_err(c32.cpu().numpy(), ref) < 2e-5
+
+
 # bf16: the automatic tile choice and each tile the stage's choice can make
 # (256x256, 256x128 and 128x192 tiles, 256x192); fp32 has one kernel.
 EPI_CASES = [("bf16", 0), ("bf16", 7), ("bf16", 8), ("bf16", 9), ("bf16", 10), ("fp32", 0)]
