@@ -36,6 +36,10 @@ SMALL = {
                                  tp_degree=1, n_sub=1, recompute_mask=0b1, seed=36),
     "min-fp32": synth.StageShape("minf", n_blocks=1, hidden=64, n_heads=1, ffn=64, seq_len=64, micro_batch=1,
                                  tp_degree=1, n_sub=1, recompute_mask=0b0, dtype="fp32", seed=37),
+    # the largest block count (64), every other block recomputed, bit 63 included
+    "max-blocks-fp32": synth.StageShape("maxl", n_blocks=64, hidden=64, n_heads=1, ffn=64, seq_len=64,
+                                        micro_batch=2, tp_degree=1, n_sub=2, recompute_mask=0xAAAAAAAAAAAAAAAA,
+                                        dtype="fp32", seed=38),
 }
 
 
