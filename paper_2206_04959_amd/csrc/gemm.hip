@@ -67,7 +67,7 @@ __device__ __forceinline__ void epilogue4(const GemmProblem& p, int m, int n, fl
         v[e] += b[e];
         g[e] = gelu_f(v[e]);
       }
-      store4(reinterpret_cast<T*>(p.aux) + off, v);
+      if (p.aux) store4(reinterpret_cast<T*>(p.aux) + off, v);
       store4(c, g);
     } else if constexpr (EPI == EPI_BIAS_RESID) {
       float b[4], r[4];
@@ -124,7 +124,7 @@ __device__ __forceinline__ void epilogue8(const GemmProblem& p, int m, int n, fl
         v[e] += b[e];
         g[e] = gelu_f(v[e]);
       }
-      store8(reinterpret_cast<T*>(p.aux) + off, v);
+      if (p.aux) store8(reinterpret_cast<T*>(p.aux) + off, v);
       store8(c, g);
     } else if constexpr (EPI == EPI_BIAS_RESID) {
       float b[8], r[8];

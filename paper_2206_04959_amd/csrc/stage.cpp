@@ -348,11 +348,16 @@ int block_forward_step(merak_stage* S, const void* params, int l, int j, int k, 
                                    P(params, S, l, P_LN2G), P(params, S, l, P_LN2B), A + L.ln2 + r0 * D.h * e,
                                    (float*)(A + L.mu2) + r0, (float*)(A + L.rs2) + r0, st, members, 2 * M));
       break;
-    case 5:  // FC1 (column parallel) + bias + GeLU; keeps the pre-activation u
+    case 5: {  // FC1 (column parallel) + bias + GeLU; keeps the pre-activation u for
+               // the GeLU backward, except in the forward of a recomputed block,
+               // whose activations (in the shared temporary area) the
+               // recomputation rebuilds
+      const bool drop_u = ((D.mask >> l) & 1) && A == S->ws + S->W.fwd_tmp;
       *p = gp(M, D.fl, D.h, A + L.ln2 + r0 * D.h * e, D.h, P(params, S, l, P_W1), D.h, A + L.g + r0 * D.fl * e, D.fl,
-              P(params, S, l, P_B1), nullptr, A + L.u + r0 * D.fl * e);
+              P(params, S, l, P_B1), nullptr, drop_u ? nullptr : A + L.u + r0 * D.fl * e);
       *epi = EPI_BIAS_GELU;
       break;
+    }
     default:  // FC2 (row parallel): partial sum -> hand-off; y = x1 + partial + b2
       *p = gp(M, D.h, D.fl, A + L.g + r0 * D.fl * e, D.fl, P(params, S, l, P_W2), D.fl, y + r0 * D.h * e, D.h,
               P(params, S, l, P_B2), A + L.x1 + r0 * D.h * e, part_f ? part_f + r0 * D.h * e : nullptr);
