@@ -831,16 +831,27 @@ int merak_stage_bwd(merak_stage_t S, const void* params, const void* dy, void* d
         }
       }
       // Parameter gradients on the internal stream once every sub-micro-
-      // batch has passed the step that makes their inputs.
-      const int part = k == 0 ? 0 : k == 4 ? 1 : k == 5 ? 3 : -1;
+      // batch has passed the step that makes their inputs.  The first block
+      // (the last one here) leaves its sums (parts 2 and 3) to the caller's
+      // streams after its chain, where they run beside the internal stream's
+      // last weight-gradient GEMM instead of after it.
+      const int part = k == 0 ? 0 : k == 4 ? 1 : (k == 5 && l > 0) ? 3 : -1;
       if (part >= 0) {
         HIP_TRY(hipEventRecord(S->ev_j0, s0));
         HIP_TRY(hipEventRecord(S->ev_j1, s1));
         HIP_TRY(hipStreamWaitEvent(S->aux, S->ev_j0, 0));
         HIP_TRY(hipStreamWaitEvent(S->aux, S->ev_j1, 0));
         TRY(block_param_grads(S, l, part, A, xin, dyl, B, d1, d2, grads, accumulate, S->aux));
-        if (part == 1) TRY(block_param_grads(S, l, 2, A, xin, dyl, B, d1, d2, grads, accumulate, S->aux));
+        if (part == 1 && l > 0) TRY(block_param_grads(S, l, 2, A, xin, dyl, B, d1, d2, grads, accumulate, S->aux));
       }
+    }
+    if (l == 0) {
+      HIP_TRY(hipEventRecord(S->ev_j0, s0));
+      HIP_TRY(hipEventRecord(S->ev_j1, s1));
+      HIP_TRY(hipStreamWaitEvent(s0, S->ev_j1, 0));
+      HIP_TRY(hipStreamWaitEvent(s1, S->ev_j0, 0));
+      TRY(block_param_grads(S, l, 2, A, xin, dyl, B, d1, d2, grads, accumulate, s1));
+      TRY(block_param_grads(S, l, 3, A, xin, dyl, B, d1, d2, grads, accumulate, s0));
     }
     HIP_TRY(hipEventRecord(S->ev_dw[par], S->aux));
   }
