@@ -463,8 +463,9 @@ int block_backward_step(merak_stage* S, const void* params, int l, int j, int k,
 // backward of every sub-micro-batch; part 1 (dW_o, dW_qkv) and part 2 (b_o,
 // b_qkv and LayerNorm 2's sums) need dx1, d_ln2 and dqkv, i.e. the attention
 // backward; part 3 (LayerNorm 1's sums) needs d_ln1, made by the QKV
-// backward.  (Splitting parts 2 and 3 leaves only LayerNorm 1's sums after
-// the last block's chain.)
+// backward.  Parts 2 and 3 of the first block, the last the backward
+// reaches, run on the caller's streams after its chains, beside part 1's
+// GEMM on the internal stream.
 int block_param_grads(merak_stage* S, int l, int group, const char* A, const char* x, const char* dy, const char* B,
                       const char* d_ln1, const char* d_ln2, float* grads, int acc, hipStream_t st) {
   const Dims& D = S->D;
